@@ -1,0 +1,114 @@
+"""Seeded synthetic inputs for the SFC-CA GEMM workloads.
+
+This module only draws numbers: it holds none of the method's arithmetic, and
+both the HIP path and the CPU oracle receive exactly the arrays it returns.
+
+Matrices are drawn in fp32 with ``numpy.random.default_rng(seed)`` and
+rounded to bf16 (round to nearest even, done by torch's CPU conversion); they
+are returned as uint16 bit patterns, row-major with a chosen leading
+dimension.  Padding columns (ld > cols) hold a NaN sentinel so that a kernel
+that reads them shows it.
+
+Workloads (the paper's shapes and roles: Section IV.A's cube sweep, the
+Llama-3-8B prefill projections of Section IV.C) are synthetic stand-ins; no
+dataset or trained weight is involved.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+from typing import List, Optional, Tuple
+
+import numpy as np
+import torch
+
+NAN_BF16 = 0x7FC0
+
+
+def _to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    t = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32))
+    return t.to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+
+
+def draw(rows: int, cols: int, dist: Tuple, seed: int, ld: Optional[int] = None) -> np.ndarray:
+    """A rows x ld uint16 array of bf16 patterns; columns >= cols are NaN.
+
+    dist is ("uniform", lo, hi), ("normal", mean, std) or ("int", lo, hi)
+    (integers drawn uniformly from [lo, hi], inclusive).
+    """
+    ld = cols if ld is None else ld
+    if ld < cols:
+        raise ValueError("ld < cols")
+    rng = np.random.default_rng(seed)
+    kind = dist[0]
+    if kind == "uniform":
+        x = rng.uniform(dist[1], dist[2], size=(rows, cols)).astype(np.float32)
+    elif kind == "normal":
+        x = rng.normal(dist[1], dist[2], size=(rows, cols)).astype(np.float32)
+    elif kind == "int":
+        x = rng.integers(dist[1], dist[2] + 1, size=(rows, cols)).astype(np.float32)
+    else:
+        raise ValueError(kind)
+    out = np.full((rows, ld), NAN_BF16, dtype=np.uint16)
+    if rows and cols:
+        out[:, :cols] = _to_bf16_bits(x)
+    return out
+
+
+@dataclass
+class Gemm:
+    M: int
+    N: int
+    K: int
+    dist_a: Tuple
+    dist_b: Tuple
+    seed_a: int
+    seed_b: int
+    out: str = "f32"                      # "f32" or "bf16"
+
+    @property
+    def flops(self) -> int:
+        return 2 * self.M * self.N * self.K
+
+    def operands(self, lda: Optional[int] = None, ldb: Optional[int] = None):
+        A = draw(self.M, self.K, self.dist_a, self.seed_a, lda)
+        B = draw(self.K, self.N, self.dist_b, self.seed_b, ldb)
+        return A, B
+
+
+@dataclass
+class Workload:
+    name: str
+    gemms: List[Gemm]
+    tile: str = "auto"                    # "auto", "128x128", "256x128", "128x256", "256x256"
+    ca_layers: List[int] = field(default_factory=lambda: [1])
+
+    @property
+    def flops(self) -> int:
+        return sum(g.flops for g in self.gemms)
+
+
+def workloads() -> List[Workload]:
+    """The five measured workloads.  Seeds: workload k draws A with 1000k+1 and
+    B with 1000k+2; GEMM j of the prefill batch uses 5000+10j+1 and +2."""
+    U = ("uniform", -1.0, 1.0)
+    return [
+        Workload("cube512_f32out_t128", [Gemm(512, 512, 512, U, U, 1001, 1002)], tile="128x128"),
+        Workload("square8192_bf16out_t256",
+                 [Gemm(8192, 8192, 8192, ("normal", 0.0, 1.0), ("normal", 0.0, 1.0), 2001, 2002,
+                       out="bf16")], tile="256x256"),
+        Workload("ragged3000x7000x2048_f32out", [Gemm(3000, 7000, 2048, U, U, 3001, 3002)]),
+        Workload("kdominant1024x1024x65536_f32out",
+                 [Gemm(1024, 1024, 65536, ("normal", 0.0, 0.1), ("normal", 0.0, 0.1), 4001, 4002)],
+                 ca_layers=[1, 2, 4, 8]),
+        Workload("prefill4096_bf16out",
+                 [Gemm(4096, n, k, ("normal", 0.0, 1.0), ("normal", 0.0, 0.02),
+                       5000 + 10 * j + 1, 5000 + 10 * j + 2, out="bf16")
+                  for j, (n, k) in enumerate([(4096, 4096), (14336, 4096), (4096, 14336)])]),
+    ]
+
+
+def workload(name: str) -> Workload:
+    for w in workloads():
+        if w.name == name:
+            return w
+    raise KeyError(name)
