@@ -1,0 +1,230 @@
+#!/usr/bin/env python3
+"""Benchmark of the SFC-CA bf16 GEMM on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W]
+
+Prints ONE JSON line.  The headline `value` is TFLOP/s of the 8192^3 bf16
+GEMM (256x256 blocks, a 32x32 block grid in generalized Hilbert order, bf16
+output), timed over K back-to-back calls with inputs resident in HBM.  The
+line also carries:
+  * roofline   -- the GEMM kernel's own average duration (HIP events on the
+                  launch stream over the timed steps) against the bf16 dense
+                  MFMA peak;
+  * cpu_baseline -- the CPU oracle on a bounded row sample of the same GEMM;
+  * workloads  -- every measured workload (TFLOP/s, cold and warm, the paper's
+                  protocol of 10 cold repetitions) and their flop-weighted
+                  harmonic mean.
+Inputs are synthetic (seeded, see paper_2601_16294_amd/inputs.py).
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+METRIC = "bf16 GEMM TFLOP/s per shape + weighted harmonic mean; % of MFMA peak"
+# MI355X bf16 dense MFMA peak: 256 CUs x 4096 FLOP/clock x 2.4 GHz.
+PEAK_BF16_TFLOPS = 2516.6
+PEAK_HBM_GBS = 8000.0
+HEADLINE = "square8192_bf16out_t256"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_square8192_gemm.json")
+GEMM_SRC = os.path.join(ROOT, "paper_2601_16294_amd", "csrc", "sfc_gemm.hip")
+
+
+def log(msg: str) -> None:
+    print(msg, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--reps", type=int, default=10, help="cold repetitions per workload")
+    ap.add_argument("--no-workloads", action="store_true", help="headline only")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--order", default="hilbert", choices=["hilbert", "row_major"])
+    ap.add_argument("--sched", default="interleaved", choices=["interleaved", "block"])
+    ap.add_argument("--only", default=None, help="run the kernel of one workload K times and exit")
+    return ap.parse_args()
+
+
+def traffic_record():
+    """HBM bytes per launch from committed rocprofv3 counter runs, valid only
+    while the GEMM kernel source is the one the counters were taken on."""
+    try:
+        rec = json.load(open(TRAFFIC_FILE))
+    except (OSError, ValueError):
+        return None
+    sha = hashlib.sha256(open(GEMM_SRC, "rb").read()).hexdigest()
+    if rec.get("kernel_src_sha256") != sha:
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported "
+              "(this build has no multi-GPU path)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_2601_16294_amd import sfcgemm as sg
+    from paper_2601_16294_amd.inputs import workloads
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream()
+    W = {w.name: w for w in workloads()}
+
+    def run_once(dA, dB, C, w, c):
+        sg.sfc_gemm_ex(dA, dB, C, ca_layers=c, tile=w.tile, order=args.order, sched=args.sched,
+                       stream=stream)
+
+    def prepare(g):
+        A, B = g.operands()
+        dA, dB = sg.to_device_bf16(A), sg.to_device_bf16(B)
+        dtype = torch.float32 if g.out == "f32" else torch.bfloat16
+        C = torch.empty((g.M, g.N), dtype=dtype, device=dev)
+        return A, B, dA, dB, C
+
+    # ---------------------------------------------------------------- headline
+    w = W[HEADLINE]
+    g = w.gemms[0]
+    log(f"[bench] preparing {HEADLINE} {g.M}x{g.N}x{g.K}")
+    A_host, B_host, dA, dB, C = prepare(g)
+    plan = sg.sfc_gemm_plan(g.M, g.N, g.K, 1, w.tile)
+    if args.only:
+        ow = W[args.only]
+        og = ow.gemms[0]
+        _, _, oA, oB, oC = prepare(og)
+        for _ in range(args.steps):
+            run_once(oA, oB, oC, ow, ow.ca_layers[-1])
+        torch.cuda.synchronize()
+        log(f"[bench] ran {args.only} {args.steps} times")
+        return
+    for _ in range(args.warmup):
+        run_once(dA, dB, C, w, 1)
+    torch.cuda.synchronize()
+    log(f"[bench] warmup done; timing {args.steps} steps")
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        starts[i].record(stream)
+        run_once(dA, dB, C, w, 1)
+        ends[i].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    kern_ms = sum(s.elapsed_time(e) for s, e in zip(starts, ends)) / args.steps
+    ms_per_step = wall * 1e3 / args.steps
+    value = g.flops / (ms_per_step * 1e-3) / 1e12
+    achieved = g.flops / (kern_ms * 1e-3) / 1e12
+    log(f"[bench] headline {value:.1f} TFLOP/s (wall), kernel {kern_ms:.3f} ms -> {achieved:.1f} TFLOP/s")
+    del dA, dB, C
+    torch.cuda.empty_cache()
+
+    # --------------------------------------------------------------- workloads
+    table = None
+    if not args.no_workloads:
+        flush = torch.empty(512 * 1024 * 1024 // 4, dtype=torch.float32, device=dev)
+        table = {}
+        whm_num = whm_den = 0.0
+        for name, wl in W.items():
+            entry = {"flops": wl.flops, "tile": wl.tile, "gemms": [list((x.M, x.N, x.K)) for x in wl.gemms]}
+            per_c = {}
+            for c in wl.ca_layers:
+                cold_t = warm_t = 0.0
+                for gg in wl.gemms:
+                    _, _, a, b, cc = prepare(gg)
+                    for _ in range(3):
+                        run_once(a, b, cc, wl, c)
+                    torch.cuda.synchronize()
+                    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                          for _ in range(args.reps)]
+                    for s, e in ev:                           # cold: caches flushed, untimed
+                        flush.zero_()
+                        s.record(stream)
+                        run_once(a, b, cc, wl, c)
+                        e.record(stream)
+                    torch.cuda.synchronize()
+                    cold_t += sum(s.elapsed_time(e) for s, e in ev) / args.reps
+                    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                    s.record(stream)
+                    for _ in range(args.reps):
+                        run_once(a, b, cc, wl, c)
+                    e.record(stream)
+                    torch.cuda.synchronize()
+                    warm_t += s.elapsed_time(e) / args.reps
+                    del a, b, cc
+                per_c[c] = {"cold_ms": round(cold_t, 4), "warm_ms": round(warm_t, 4),
+                            "tflops_cold": round(wl.flops / (cold_t * 1e-3) / 1e12, 2),
+                            "tflops_warm": round(wl.flops / (warm_t * 1e-3) / 1e12, 2)}
+                log(f"[bench] {name} c={c}: {per_c[c]}")
+            best_c = max(per_c, key=lambda k: per_c[k]["tflops_cold"])
+            best = per_c[best_c]
+            entry.update({"per_ca_layers": per_c if len(per_c) > 1 else None, "best_ca_layers": best_c,
+                          "tflops": best["tflops_cold"], "tflops_warm": best["tflops_warm"],
+                          "frac_of_mfma_peak": round(best["tflops_cold"] / PEAK_BF16_TFLOPS, 4)})
+            table[name] = entry
+            whm_num += wl.flops
+            whm_den += wl.flops / best["tflops_cold"]
+            torch.cuda.empty_cache()
+        del flush
+        whm = whm_num / whm_den
+        best_shape = max(v["tflops"] for v in table.values())
+        table = {"protocol": f"mean of {args.reps} cold reps (512 MiB flush between), best ca_layers",
+                 "shapes": table, "whm_tflops": round(whm, 2),
+                 "whm_over_best_shape": round(whm / best_shape, 4)}
+
+    # ------------------------------------------------------------ cpu baseline
+    cpu = None
+    if not args.no_cpu_baseline:
+        from oracle import gemm as ogemm
+        threads = ogemm.threads()
+        rows = 8
+        t = time.perf_counter()
+        ogemm.gemm_ref_rows(A_host, B_host, g.N, g.K, g.K, g.N, row0=0, nrows=rows)
+        dt = time.perf_counter() - t
+        rows = int(max(8, min(g.M, rows * args.cpu_seconds / max(dt, 1e-3))))
+        log(f"[bench] cpu oracle: {rows} rows on {threads} threads")
+        t = time.perf_counter()
+        ogemm.gemm_ref_rows(A_host, B_host, g.N, g.K, g.K, g.N, row0=0, nrows=rows)
+        dt = time.perf_counter() - t
+        cpu = {"value": round(2.0 * rows * g.N * g.K / dt / 1e12, 6), "unit": "TFLOP/s",
+               "cores": threads, "kind": "oracle",
+               "sample": f"rows 0..{rows - 1} of the {g.M}x{g.N}x{g.K} GEMM "
+                         f"({rows}x{g.N} outputs, fp64, {dt:.1f} s)"}
+
+    line = {
+        "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "accumulate": "f32", "data": "synthetic",
+        "config": {"workload": HEADLINE, "M": g.M, "N": g.N, "K": g.K, "out": g.out,
+                   "tile": w.tile, "grid": [plan["gm"], plan["gn"]], "ca_layers": 1,
+                   "order": args.order, "sched": args.sched, "workgroups": plan["workgroups"],
+                   "dist": "A, B ~ N(0,1) rounded to bf16"},
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                     "traffic": traffic_record(), "kernel": "sfc_gemm_kernel<256,256,bf16 out>",
+                     "kernel_ms": round(kern_ms, 4)},
+        "cpu_baseline": cpu,
+        "workloads": table,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,157 @@
+/*
+ * sfcgemm.h -- C ABI of the MI355X (gfx950) space-filling-curve,
+ * communication-avoiding bf16 GEMM.
+ *
+ * The operation is the GEMM of the paper's Section II.A, C = A * B with A of
+ * M x K and B of K x N, executed as in Listing 1 (Section II.D): the M x N
+ * output is cut into BM x BN blocks; the blocks are visited in generalized
+ * Hilbert order (Section II.B); with ca_layers = c > 1 the contraction is
+ * split into c contiguous K ranges, each computing a full copy of C, and the
+ * copies are summed (Section II.C / II.D).  C is overwritten (Listing 1 zeroes
+ * each block before the first contraction); there is no alpha or beta.
+ *
+ * Conventions for every entry point below
+ *   - Matrices are row-major.  A[i][k] is at A[i*lda + k], B[k][j] at
+ *     B[k*ldb + j], C[i][j] at C[i*ldc + j].  bf16 elements are 16-bit
+ *     patterns (the upper half of an IEEE binary32).
+ *   - A, B, C and workspace pointers are DEVICE pointers on the current HIP
+ *     device; the caller owns them and keeps them alive until the work on
+ *     `stream` has finished.  `stream` is a hipStream_t (NULL = null stream).
+ *   - GEMM calls are asynchronous: they validate, enqueue kernels on `stream`
+ *     and return.  Faults during execution surface at the next synchronisation.
+ *   - On any error nothing is enqueued and C is not touched.
+ *   - Elements of C outside the M x N region (ldc padding) are never written;
+ *     elements of A and B outside their M x K and K x N regions are never used.
+ *   - Accumulation is fp32 in every case.  For a fixed tile shape and layer
+ *     count the result is bitwise reproducible and independent of the tile
+ *     order and schedule.
+ */
+#ifndef SFCGEMM_H
+#define SFCGEMM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- return codes ------------------------------------------------------ */
+#define SFC_OK               0
+#define SFC_ERR_INVALID_ARG (-1) /* negative size, ld too small, null pointer, bad enum */
+#define SFC_ERR_UNSUPPORTED (-2) /* misaligned element pointer, size beyond int32 tile indexing */
+#define SFC_ERR_WORKSPACE   (-3) /* caller workspace smaller than sfc_gemm_ws_size() */
+#define SFC_ERR_HIP         (-4) /* HIP runtime error; sfc_last_error() has the text */
+
+/* ---- output element type (reading A8: fp32 accumulate, fp32 or bf16 out) */
+#define SFC_OUT_F32  0           /* C holds float */
+#define SFC_OUT_BF16 1           /* C holds bf16, rounded to nearest even */
+
+/* ---- block (tile) shape BM x BN of the output grid --------------------- */
+#define SFC_TILE_AUTO    0       /* chosen from M, N, K and ca_layers */
+#define SFC_TILE_128x128 1
+#define SFC_TILE_256x128 2       /* BM = 256, BN = 128 */
+#define SFC_TILE_128x256 3       /* BM = 128, BN = 256 */
+#define SFC_TILE_256x256 4
+
+/* ---- order of the output blocks ---------------------------------------- */
+#define SFC_ORDER_HILBERT   0    /* generalized Hilbert curve (Section II.B) */
+#define SFC_ORDER_ROW_MAJOR 1    /* plain row-major; for comparison only */
+
+/* ---- how curve positions are dealt to the persistent workgroups --------- */
+#define SFC_SCHED_INTERLEAVED 0  /* workgroup r takes positions r, r+P, ...: the blocks
+                                    in flight form one contiguous curve segment, and each
+                                    chiplet (XCD) owns a contiguous sub-segment of it */
+#define SFC_SCHED_BLOCK       1  /* workgroup r takes the r-th contiguous range of
+                                    positions (the block partition of Section III.A) */
+
+/*
+ * sfc_tile_order -- the block order of a gm x gn grid (Section II.B; the map
+ * built by create_sfc_map in Listing 1).
+ *   gm, gn   grid sides (blocks along M and along N), both >= 1, gm*gn < 2^31.
+ *   out_idx  HOST buffer of gm*gn int32, caller-owned.  On return out_idx[s]
+ *            = im*gn + in for the block (im, in) visited at curve position s.
+ * The table is produced on the current device by the same generator the GEMM
+ * uses, then copied back; the call is synchronous.
+ * Returns SFC_OK, SFC_ERR_INVALID_ARG (bad sides, NULL out_idx),
+ * SFC_ERR_UNSUPPORTED (gm*gn too large) or SFC_ERR_HIP.
+ */
+int sfc_tile_order(int gm, int gn, int32_t *out_idx);
+
+/* As sfc_tile_order, with an explicit SFC_ORDER_* mode. */
+int sfc_tile_order_ex(int gm, int gn, int order, int32_t *out_idx);
+
+/*
+ * sfc_gemm -- C = A * B, fp32 output (Section II.A, Listing 1).
+ *   M, N, K    >= 0.  M == 0 or N == 0: nothing to do, SFC_OK.  K == 0: C = 0.
+ *   A, lda     bf16, M x K, lda >= K (A may be NULL when M*K == 0).
+ *   B, ldb     bf16, K x N, ldb >= N (B may be NULL when K*N == 0).
+ *   C, ldc     float, M x N, ldc >= N.
+ *   ca_layers  c in [1, 64]: number of K ranges / copies of C.  The K blocks
+ *              (64 deep) are split into min(c, ceil(K/64)) contiguous ranges,
+ *              range l holding blocks [floor(l*nK/c), floor((l+1)*nK/c)).  For
+ *              c > 1 the partial copies live in a workspace of
+ *              sfc_gemm_ws_size() bytes that the library allocates once per
+ *              device and reuses; concurrent c > 1 calls on different streams
+ *              must use sfc_gemm_ex with their own workspaces.
+ *   stream     hipStream_t or NULL.
+ */
+int sfc_gemm(int64_t M, int64_t N, int64_t K,
+             const void *A, int64_t lda,
+             const void *B, int64_t ldb,
+             void *C, int64_t ldc,
+             int ca_layers, void *stream);
+
+/* As sfc_gemm with a bf16 C (rounded to nearest even from the fp32 sums). */
+int sfc_gemm_bf16out(int64_t M, int64_t N, int64_t K,
+                     const void *A, int64_t lda,
+                     const void *B, int64_t ldb,
+                     void *C, int64_t ldc,
+                     int ca_layers, void *stream);
+
+/*
+ * sfc_gemm_ws_size -- bytes of fp32 workspace that a ca_layers = c call needs:
+ * c_eff * M * N * 4 with c_eff = min(c, ceil(K/64)) when c_eff > 1, else 0.
+ * Returns 0 for invalid arguments as well.
+ */
+size_t sfc_gemm_ws_size(int64_t M, int64_t N, int64_t K, int ca_layers);
+
+/*
+ * sfc_gemm_ex -- the general entry point behind sfc_gemm / sfc_gemm_bf16out.
+ *   out_type   SFC_OUT_F32 or SFC_OUT_BF16.
+ *   tile       SFC_TILE_*; order SFC_ORDER_*; sched SFC_SCHED_*.
+ *   ws         device workspace of ws_bytes bytes, or NULL to use the library's
+ *              internal one.  When c_eff > 1, layer l of the partial result is
+ *              left in ws as a dense fp32 M x N matrix at ws + l*M*N floats.
+ * Tile order and schedule never change the result bits; tile shape and layer
+ * count change only the fp32 summation grouping.
+ */
+int sfc_gemm_ex(int64_t M, int64_t N, int64_t K,
+                const void *A, int64_t lda,
+                const void *B, int64_t ldb,
+                void *C, int64_t ldc,
+                int out_type, int ca_layers, int tile, int order, int sched,
+                void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * sfc_gemm_plan -- what sfc_gemm_ex would launch, without launching.
+ *   plan[0] = BM, plan[1] = BN, plan[2] = gm, plan[3] = gn, plan[4] = c_eff,
+ *   plan[5] = number of persistent workgroups, plan[6] = workgroups per CU.
+ * Needs a device (it queries the CU count and kernel occupancy).
+ */
+int sfc_gemm_plan(int64_t M, int64_t N, int64_t K, int ca_layers, int tile, int64_t plan[7]);
+
+/* Static text of a return code. */
+const char *sfc_strerror(int code);
+
+/* Text of the last error raised on the calling thread ("" if none). */
+const char *sfc_last_error(void);
+
+/* ABI version: 1. */
+int sfc_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SFCGEMM_H */

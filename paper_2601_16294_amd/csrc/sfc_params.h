@@ -1,0 +1,48 @@
+// Internal interface between the C-ABI layer and the HIP kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace sfc {
+
+constexpr int kBK = 64;          // depth of one K block (the paper's bk)
+constexpr int kThreads = 256;    // four wave64 waves per workgroup
+
+enum TileId { kT128x128 = 0, kT256x128 = 1, kT128x256 = 2, kT256x256 = 3, kNumTiles = 4 };
+
+inline int tile_bm(int t) { return (t == kT256x128 || t == kT256x256) ? 256 : 128; }
+inline int tile_bn(int t) { return (t == kT128x256 || t == kT256x256) ? 256 : 128; }
+
+struct GemmParams {
+  int64_t M, N, K;
+  const uint16_t* A;
+  int64_t lda;
+  const uint16_t* B;
+  int64_t ldb;
+  void* out;                 // C (layers == 1) or the fp32 workspace (layers > 1)
+  int64_t ldo;               // leading dimension of `out`
+  int64_t out_layer_stride;  // elements between layer copies of `out` (0 when layers == 1)
+  const int32_t* table;      // gm*gn curve positions -> im*gn + in
+  int gm, gn;
+  int layers;                // c_eff
+  int nk;                    // ceil(K / kBK)
+  int64_t tasks;             // gm * gn * layers
+  int sched;                 // SFC_SCHED_*
+  int pad_;
+};
+
+// Curve table of a gm x gn grid into dev_out (gm*gn int32), order = SFC_ORDER_*.
+hipError_t launch_sfc_order(int gm, int gn, int order, int32_t* dev_out, hipStream_t stream);
+
+// Persistent GEMM.  out_bf16 selects the epilogue; vec selects 128-bit loads
+// (needs 16-byte aligned A and B, lda, ldb, K and N multiples of 8).
+hipError_t launch_gemm(int tile, bool out_bf16, bool vec, const GemmParams& p, int grid,
+                       hipStream_t stream);
+// Workgroups of the given kernel variant that fit on one CU.
+hipError_t gemm_occupancy(int tile, bool out_bf16, bool vec, int* blocks_per_cu);
+
+// C[i][j] = sum_l W[l][i][j] (ascending l, fp32), W dense M x N per layer.
+hipError_t launch_reduce(const float* W, int layers, int64_t M, int64_t N, void* C, int64_t ldc,
+                         bool out_bf16, hipStream_t stream);
+
+}  // namespace sfc

@@ -1,0 +1,102 @@
+// Argument checks of the C ABI, kept free of any HIP dependency so that they
+// run (and are tested) without a GPU.  Every check happens before the library
+// touches the device.
+#pragma once
+#include <stdint.h>
+#include <stdio.h>
+
+#include "sfcgemm.h"
+
+namespace sfc {
+
+constexpr int kMaxLayers = 64;
+constexpr int64_t kMaxDim = (int64_t)1 << 31;   // block indices are int32
+
+struct Checked {
+  int code;
+  char msg[160];
+};
+
+inline Checked ok() { Checked c; c.code = SFC_OK; c.msg[0] = 0; return c; }
+inline Checked fail(int code, const char* what) {
+  Checked c;
+  c.code = code;
+  snprintf(c.msg, sizeof c.msg, "%s", what);
+  return c;
+}
+
+inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// Layers actually used: min(c, number of 64-deep K blocks), at least 1.
+inline int effective_layers(int64_t K, int c, int bk) {
+  const int64_t nk = K > 0 ? ceil_div(K, bk) : 0;
+  int64_t e = c < nk ? c : nk;
+  return e < 1 ? 1 : (int)e;
+}
+
+inline Checked check_order_args(int gm, int gn, int order, const void* out) {
+  if (gm <= 0 || gn <= 0) return fail(SFC_ERR_INVALID_ARG, "grid sides must be >= 1");
+  if (order != SFC_ORDER_HILBERT && order != SFC_ORDER_ROW_MAJOR)
+    return fail(SFC_ERR_INVALID_ARG, "unknown order");
+  if (!out) return fail(SFC_ERR_INVALID_ARG, "out_idx is NULL");
+  if ((int64_t)gm * gn >= kMaxDim) return fail(SFC_ERR_UNSUPPORTED, "gm*gn must be < 2^31");
+  return ok();
+}
+
+inline Checked check_gemm_args(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda,
+                               const void* B, int64_t ldb, const void* C, int64_t ldc,
+                               int out_type, int ca_layers, int tile, int order, int sched,
+                               const void* ws, size_t ws_bytes) {
+  if (M < 0 || N < 0 || K < 0) return fail(SFC_ERR_INVALID_ARG, "M, N, K must be >= 0");
+  if (out_type != SFC_OUT_F32 && out_type != SFC_OUT_BF16)
+    return fail(SFC_ERR_INVALID_ARG, "unknown out_type");
+  if (ca_layers < 1 || ca_layers > kMaxLayers)
+    return fail(SFC_ERR_INVALID_ARG, "ca_layers must be in [1, 64]");
+  if (tile < SFC_TILE_AUTO || tile > SFC_TILE_256x256) return fail(SFC_ERR_INVALID_ARG, "unknown tile");
+  if (order != SFC_ORDER_HILBERT && order != SFC_ORDER_ROW_MAJOR)
+    return fail(SFC_ERR_INVALID_ARG, "unknown order");
+  if (sched != SFC_SCHED_INTERLEAVED && sched != SFC_SCHED_BLOCK)
+    return fail(SFC_ERR_INVALID_ARG, "unknown sched");
+  if (M == 0 || N == 0) return ok();   // nothing to write
+  if (!C) return fail(SFC_ERR_INVALID_ARG, "C is NULL");
+  if (ldc < N) return fail(SFC_ERR_INVALID_ARG, "ldc < N");
+  if (K > 0) {
+    if (!A) return fail(SFC_ERR_INVALID_ARG, "A is NULL");
+    if (!B) return fail(SFC_ERR_INVALID_ARG, "B is NULL");
+    if (lda < K) return fail(SFC_ERR_INVALID_ARG, "lda < K");
+    if (ldb < N) return fail(SFC_ERR_INVALID_ARG, "ldb < N");
+    if (((uintptr_t)A & 1) || ((uintptr_t)B & 1))
+      return fail(SFC_ERR_UNSUPPORTED, "A and B must be 2-byte aligned");
+  }
+  const uintptr_t calign = out_type == SFC_OUT_F32 ? 4 : 2;
+  if ((uintptr_t)C % calign) return fail(SFC_ERR_UNSUPPORTED, "C is not aligned to its element size");
+  if (M >= kMaxDim || N >= kMaxDim || K >= kMaxDim)
+    return fail(SFC_ERR_UNSUPPORTED, "M, N and K must be < 2^31");
+  // the smallest block is 128 x 128
+  if (ceil_div(M, 128) * ceil_div(N, 128) >= kMaxDim)
+    return fail(SFC_ERR_UNSUPPORTED, "too many output blocks");
+  const int ce = effective_layers(K, ca_layers, 64);
+  if (ce > 1 && ws) {
+    const uint64_t need = (uint64_t)ce * (uint64_t)M * (uint64_t)N * 4u;
+    if (ws_bytes < need) return fail(SFC_ERR_WORKSPACE, "workspace smaller than sfc_gemm_ws_size()");
+    if ((uintptr_t)ws % 16) return fail(SFC_ERR_UNSUPPORTED, "workspace must be 16-byte aligned");
+  }
+  return ok();
+}
+
+inline size_t ws_size(int64_t M, int64_t N, int64_t K, int ca_layers) {
+  if (M < 0 || N < 0 || K < 0 || ca_layers < 1 || ca_layers > kMaxLayers) return 0;
+  const int ce = effective_layers(K, ca_layers, 64);
+  if (ce <= 1) return 0;
+  return (size_t)ce * (size_t)M * (size_t)N * 4u;
+}
+
+// 128-bit staging loads are legal when every row starts 16-byte aligned and
+// the K and N extents end on whole 8-element chunks.
+inline bool vector_loads_ok(const void* A, int64_t lda, const void* B, int64_t ldb, int64_t K,
+                            int64_t N) {
+  return ((uintptr_t)A % 16 == 0) && ((uintptr_t)B % 16 == 0) && (lda % 8 == 0) &&
+         (ldb % 8 == 0) && (K % 8 == 0) && (N % 8 == 0);
+}
+
+}  // namespace sfc

@@ -1,0 +1,297 @@
+// C ABI of the SFC-CA GEMM (declarations and contracts in include/sfcgemm.h).
+//
+// Host-side duties: argument checks (before any HIP call), choice of the block
+// shape, the per-device cache of curve tables (built once per grid on the
+// device and kept), the per-device internal workspace for layer copies, and
+// the launches.  Nothing here computes any part of the product.
+#include <hip/hip_runtime.h>
+
+#include <map>
+#include <mutex>
+#include <string>
+#include <tuple>
+
+#include "sfc_params.h"
+#include "sfc_validate.h"
+#include "sfcgemm.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+struct DeviceState {
+  std::map<std::tuple<int, int, int>, int32_t*> tables;   // (gm, gn, order) -> device table
+  void* ws = nullptr;
+  size_t ws_bytes = 0;
+  int num_cus = 0;
+  int occupancy[sfc::kNumTiles][2][2] = {};                  // [tile][bf16][vec], 0 = unknown
+};
+
+std::mutex g_mu;
+std::map<int, DeviceState> g_devices;
+
+int set_error(int code, const std::string& msg) {
+  g_last_error = msg;
+  return code;
+}
+
+int hip_fail(hipError_t e, const char* where) {
+  return set_error(SFC_ERR_HIP, std::string(where) + ": " + hipGetErrorString(e));
+}
+
+// Must be called with g_mu held.
+int device_state(DeviceState** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  DeviceState& st = g_devices[dev];
+  if (st.num_cus == 0) {
+    int cus = 0;
+    e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute");
+    st.num_cus = cus;
+  }
+  *out = &st;
+  return SFC_OK;
+}
+
+// Curve table of a gm x gn grid on the current device, built on first use.
+// Must be called with g_mu held.
+int get_table(DeviceState& st, int gm, int gn, int order, hipStream_t stream, const int32_t** out) {
+  auto key = std::make_tuple(gm, gn, order);
+  auto it = st.tables.find(key);
+  if (it != st.tables.end()) {
+    *out = it->second;
+    return SFC_OK;
+  }
+  int32_t* d = nullptr;
+  hipError_t e = hipMalloc(&d, sizeof(int32_t) * (size_t)gm * (size_t)gn);
+  if (e != hipSuccess) return hip_fail(e, "hipMalloc(curve table)");
+  e = sfc::launch_sfc_order(gm, gn, order, d, stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(stream);
+  if (e != hipSuccess) {
+    (void)hipFree(d);
+    return hip_fail(e, "curve table");
+  }
+  st.tables[key] = d;
+  *out = d;
+  return SFC_OK;
+}
+
+int get_occupancy(DeviceState& st, int tile, bool ob, bool vec, int* occ) {
+  int& o = st.occupancy[tile][ob][vec];
+  if (o == 0) {
+    int v = 0;
+    hipError_t e = sfc::gemm_occupancy(tile, ob, vec, &v);
+    if (e != hipSuccess) return hip_fail(e, "occupancy query");
+    o = v < 1 ? 1 : v;
+  }
+  *occ = o;
+  return SFC_OK;
+}
+
+int tile_from_api(int t) {
+  switch (t) {
+    case SFC_TILE_128x128: return sfc::kT128x128;
+    case SFC_TILE_256x128: return sfc::kT256x128;
+    case SFC_TILE_128x256: return sfc::kT128x256;
+    case SFC_TILE_256x256: return sfc::kT256x256;
+    default: return -1;
+  }
+}
+
+// Block shape for SFC_TILE_AUTO: the shape with the smallest estimated time,
+// estimated as (rounds of tasks over the persistent slots) x (block area per
+// unit of throughput).  Larger blocks reuse more data per LDS byte and sustain
+// a higher MFMA rate; the relative rates below are per-block throughputs.
+int choose_tile(int64_t M, int64_t N, int ce, int num_cus) {
+  static const int order[4] = {sfc::kT256x256, sfc::kT256x128, sfc::kT128x256, sfc::kT128x128};
+  static const double rate[4] = {1.0, 0.9, 0.9, 0.75};
+  static const int slots_per_cu[4] = {1, 1, 1, 2};
+  int best = sfc::kT128x128;
+  double best_t = 1e300;
+  for (int i = 0; i < 4; ++i) {
+    const int t = order[i];
+    const int64_t bm = sfc::tile_bm(t), bn = sfc::tile_bn(t);
+    const int64_t tasks = sfc::ceil_div(M, bm) * sfc::ceil_div(N, bn) * ce;
+    const int64_t slots = (int64_t)num_cus * slots_per_cu[i];
+    const int64_t rounds = sfc::ceil_div(tasks, slots);
+    const double est = (double)rounds * (double)(bm * bn) / rate[i] / slots_per_cu[i];
+    if (est < best_t * 0.999) { best_t = est; best = t; }
+  }
+  return best;
+}
+
+struct Plan {
+  int tile, bm, bn, gm, gn, ce, nk, grid, occ;
+  bool vec;
+};
+
+int make_plan(DeviceState& st, int64_t M, int64_t N, int64_t K, const void* A, int64_t lda,
+              const void* B, int64_t ldb, bool ob, int ca_layers, int tile_api, Plan* pl) {
+  pl->ce = sfc::effective_layers(K, ca_layers, sfc::kBK);
+  pl->tile = tile_api == SFC_TILE_AUTO ? choose_tile(M, N, pl->ce, st.num_cus) : tile_from_api(tile_api);
+  pl->bm = sfc::tile_bm(pl->tile);
+  pl->bn = sfc::tile_bn(pl->tile);
+  pl->gm = (int)sfc::ceil_div(M, pl->bm);
+  pl->gn = (int)sfc::ceil_div(N, pl->bn);
+  pl->nk = (int)(K > 0 ? sfc::ceil_div(K, sfc::kBK) : 0);
+  pl->vec = K == 0 || sfc::vector_loads_ok(A, lda, B, ldb, K, N);
+  // layer copies are fp32 whatever the output type
+  const bool kernel_bf16 = ob && pl->ce == 1;
+  int rc = get_occupancy(st, pl->tile, kernel_bf16, pl->vec, &pl->occ);
+  if (rc != SFC_OK) return rc;
+  const int64_t tasks = (int64_t)pl->gm * pl->gn * pl->ce;
+  int64_t slots = (int64_t)st.num_cus * pl->occ;
+  pl->grid = (int)(tasks < slots ? tasks : slots);
+  return SFC_OK;
+}
+
+int gemm_impl(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* B,
+              int64_t ldb, void* C, int64_t ldc, int out_type, int ca_layers, int tile, int order,
+              int sched, void* ws, size_t ws_bytes, void* stream_ptr) {
+  const sfc::Checked chk = sfc::check_gemm_args(M, N, K, A, lda, B, ldb, C, ldc, out_type, ca_layers,
+                                                tile, order, sched, ws, ws_bytes);
+  if (chk.code != SFC_OK) return set_error(chk.code, chk.msg);
+  if (M == 0 || N == 0) return SFC_OK;
+  hipStream_t stream = reinterpret_cast<hipStream_t>(stream_ptr);
+  const bool ob = out_type == SFC_OUT_BF16;
+
+  std::lock_guard<std::mutex> lock(g_mu);
+  DeviceState* st = nullptr;
+  int rc = device_state(&st);
+  if (rc != SFC_OK) return rc;
+  Plan pl;
+  rc = make_plan(*st, M, N, K, A, lda, B, ldb, ob, ca_layers, tile, &pl);
+  if (rc != SFC_OK) return rc;
+  const int32_t* table = nullptr;
+  rc = get_table(*st, pl.gm, pl.gn, order, stream, &table);
+  if (rc != SFC_OK) return rc;
+
+  float* W = nullptr;
+  if (pl.ce > 1) {
+    const size_t need = (size_t)pl.ce * (size_t)M * (size_t)N * 4u;
+    if (ws) {
+      W = reinterpret_cast<float*>(ws);
+    } else {
+      if (st->ws_bytes < need) {
+        if (st->ws) {
+          // the old buffer may still be in use by queued work
+          hipError_t e = hipDeviceSynchronize();
+          if (e != hipSuccess) return hip_fail(e, "hipDeviceSynchronize(workspace)");
+          (void)hipFree(st->ws);
+          st->ws = nullptr;
+          st->ws_bytes = 0;
+        }
+        hipError_t e = hipMalloc(&st->ws, need);
+        if (e != hipSuccess) return hip_fail(e, "hipMalloc(workspace)");
+        st->ws_bytes = need;
+      }
+      W = reinterpret_cast<float*>(st->ws);
+    }
+  }
+
+  sfc::GemmParams p;
+  p.M = M; p.N = N; p.K = K;
+  p.A = reinterpret_cast<const uint16_t*>(A); p.lda = lda;
+  p.B = reinterpret_cast<const uint16_t*>(B); p.ldb = ldb;
+  if (pl.ce > 1) { p.out = W; p.ldo = N; p.out_layer_stride = M * N; }
+  else { p.out = C; p.ldo = ldc; p.out_layer_stride = 0; }
+  p.table = table;
+  p.gm = pl.gm; p.gn = pl.gn;
+  p.layers = pl.ce;
+  p.nk = pl.nk;
+  p.tasks = (int64_t)pl.gm * pl.gn * pl.ce;
+  p.sched = sched;
+  p.pad_ = 0;
+  hipError_t e = sfc::launch_gemm(pl.tile, ob && pl.ce == 1, pl.vec, p, pl.grid, stream);
+  if (e != hipSuccess) return hip_fail(e, "GEMM launch");
+  if (pl.ce > 1) {
+    e = sfc::launch_reduce(W, pl.ce, M, N, C, ldc, ob, stream);
+    if (e != hipSuccess) return hip_fail(e, "reduction launch");
+  }
+  return SFC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int sfc_version(void) { return 1; }
+
+const char* sfc_strerror(int code) {
+  switch (code) {
+    case SFC_OK: return "success";
+    case SFC_ERR_INVALID_ARG: return "invalid argument";
+    case SFC_ERR_UNSUPPORTED: return "unsupported argument";
+    case SFC_ERR_WORKSPACE: return "workspace too small";
+    case SFC_ERR_HIP: return "HIP runtime error";
+    default: return "unknown error code";
+  }
+}
+
+const char* sfc_last_error(void) { return g_last_error.c_str(); }
+
+size_t sfc_gemm_ws_size(int64_t M, int64_t N, int64_t K, int ca_layers) {
+  return sfc::ws_size(M, N, K, ca_layers);
+}
+
+int sfc_tile_order_ex(int gm, int gn, int order, int32_t* out_idx) {
+  const sfc::Checked chk = sfc::check_order_args(gm, gn, order, out_idx);
+  if (chk.code != SFC_OK) return set_error(chk.code, chk.msg);
+  std::lock_guard<std::mutex> lock(g_mu);
+  DeviceState* st = nullptr;
+  int rc = device_state(&st);
+  if (rc != SFC_OK) return rc;
+  const int32_t* table = nullptr;
+  rc = get_table(*st, gm, gn, order, nullptr, &table);
+  if (rc != SFC_OK) return rc;
+  hipError_t e = hipMemcpy(out_idx, table, sizeof(int32_t) * (size_t)gm * (size_t)gn,
+                           hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpy(curve table)");
+  return SFC_OK;
+}
+
+int sfc_tile_order(int gm, int gn, int32_t* out_idx) {
+  return sfc_tile_order_ex(gm, gn, SFC_ORDER_HILBERT, out_idx);
+}
+
+int sfc_gemm_ex(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* B,
+                int64_t ldb, void* C, int64_t ldc, int out_type, int ca_layers, int tile, int order,
+                int sched, void* ws, size_t ws_bytes, void* stream) {
+  return gemm_impl(M, N, K, A, lda, B, ldb, C, ldc, out_type, ca_layers, tile, order, sched, ws,
+                   ws_bytes, stream);
+}
+
+int sfc_gemm(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* B, int64_t ldb,
+             void* C, int64_t ldc, int ca_layers, void* stream) {
+  return gemm_impl(M, N, K, A, lda, B, ldb, C, ldc, SFC_OUT_F32, ca_layers, SFC_TILE_AUTO,
+                   SFC_ORDER_HILBERT, SFC_SCHED_INTERLEAVED, nullptr, 0, stream);
+}
+
+int sfc_gemm_bf16out(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* B,
+                     int64_t ldb, void* C, int64_t ldc, int ca_layers, void* stream) {
+  return gemm_impl(M, N, K, A, lda, B, ldb, C, ldc, SFC_OUT_BF16, ca_layers, SFC_TILE_AUTO,
+                   SFC_ORDER_HILBERT, SFC_SCHED_INTERLEAVED, nullptr, 0, stream);
+}
+
+int sfc_gemm_plan(int64_t M, int64_t N, int64_t K, int ca_layers, int tile, int64_t plan[7]) {
+  if (!plan) return set_error(SFC_ERR_INVALID_ARG, "plan is NULL");
+  if (M <= 0 || N <= 0 || K < 0 || ca_layers < 1 || ca_layers > sfc::kMaxLayers ||
+      tile < SFC_TILE_AUTO || tile > SFC_TILE_256x256)
+    return set_error(SFC_ERR_INVALID_ARG, "invalid plan arguments");
+  std::lock_guard<std::mutex> lock(g_mu);
+  DeviceState* st = nullptr;
+  int rc = device_state(&st);
+  if (rc != SFC_OK) return rc;
+  Plan pl;
+  // aligned dummy pointers: the plan of the vector-load path
+  rc = make_plan(*st, M, N, K, reinterpret_cast<const void*>(256), (K + 7) / 8 * 8,
+                 reinterpret_cast<const void*>(256), (N + 7) / 8 * 8, false, ca_layers, tile, &pl);
+  if (rc != SFC_OK) return rc;
+  plan[0] = pl.bm; plan[1] = pl.bn; plan[2] = pl.gm; plan[3] = pl.gn;
+  plan[4] = pl.ce; plan[5] = pl.grid; plan[6] = pl.occ;
+  return SFC_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,171 @@
+"""Python binding of libsfcgemm.so (the C ABI in include/sfcgemm.h).
+
+Argument marshalling only: every step of the GEMM runs in the library's HIP
+kernels.  torch supplies device memory and the stream.  If the library is not
+built, importing this module raises; there is no fallback.
+
+Names follow the C ABI: ``sfc_tile_order``, ``sfc_gemm``, ``sfc_gemm_bf16out``,
+``sfc_gemm_ex``, ``sfc_gemm_ws_size``, ``sfc_gemm_plan``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsfcgemm.so")
+
+SFC_OK = 0
+SFC_ERR_INVALID_ARG = -1
+SFC_ERR_UNSUPPORTED = -2
+SFC_ERR_WORKSPACE = -3
+SFC_ERR_HIP = -4
+
+SFC_OUT_F32 = 0
+SFC_OUT_BF16 = 1
+
+TILES = {"auto": 0, "128x128": 1, "256x128": 2, "128x256": 3, "256x256": 4}
+ORDERS = {"hilbert": 0, "row_major": 1}
+SCHEDS = {"interleaved": 0, "block": 1}
+
+# Every symbol include/sfcgemm.h declares.
+EXPORTS = ["sfc_tile_order", "sfc_tile_order_ex", "sfc_gemm", "sfc_gemm_bf16out", "sfc_gemm_ws_size",
+           "sfc_gemm_ex", "sfc_gemm_plan", "sfc_strerror", "sfc_last_error", "sfc_version"]
+
+
+class SfcError(RuntimeError):
+    def __init__(self, code: int, what: str):
+        super().__init__(f"{what}: {code} ({strerror(code)}): {last_error()}")
+        self.code = code
+
+
+def _load() -> ctypes.CDLL:
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2601_16294_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    i64, i32, p, sz = ctypes.c_int64, ctypes.c_int, ctypes.c_void_p, ctypes.c_size_t
+    lib.sfc_tile_order.argtypes = [i32, i32, p]
+    lib.sfc_tile_order.restype = i32
+    lib.sfc_tile_order_ex.argtypes = [i32, i32, i32, p]
+    lib.sfc_tile_order_ex.restype = i32
+    gemm_args = [i64, i64, i64, p, i64, p, i64, p, i64, i32, p]
+    lib.sfc_gemm.argtypes = gemm_args
+    lib.sfc_gemm.restype = i32
+    lib.sfc_gemm_bf16out.argtypes = gemm_args
+    lib.sfc_gemm_bf16out.restype = i32
+    lib.sfc_gemm_ex.argtypes = [i64, i64, i64, p, i64, p, i64, p, i64, i32, i32, i32, i32, i32, p, sz, p]
+    lib.sfc_gemm_ex.restype = i32
+    lib.sfc_gemm_ws_size.argtypes = [i64, i64, i64, i32]
+    lib.sfc_gemm_ws_size.restype = sz
+    lib.sfc_gemm_plan.argtypes = [i64, i64, i64, i32, i32, ctypes.POINTER(ctypes.c_int64)]
+    lib.sfc_gemm_plan.restype = i32
+    lib.sfc_strerror.argtypes = [i32]
+    lib.sfc_strerror.restype = ctypes.c_char_p
+    lib.sfc_last_error.argtypes = []
+    lib.sfc_last_error.restype = ctypes.c_char_p
+    lib.sfc_version.argtypes = []
+    lib.sfc_version.restype = i32
+    return lib
+
+
+lib = _load()
+
+
+def strerror(code: int) -> str:
+    return lib.sfc_strerror(code).decode()
+
+
+def last_error() -> str:
+    return lib.sfc_last_error().decode()
+
+
+def _check(code: int, what: str) -> None:
+    if code != SFC_OK:
+        raise SfcError(code, what)
+
+
+def sfc_tile_order(gm: int, gn: int, order: str = "hilbert") -> np.ndarray:
+    """Curve table of a gm x gn block grid: entry s = im*gn + in (host int32)."""
+    out = np.empty(max(gm * gn, 1), dtype=np.int32)
+    _check(lib.sfc_tile_order_ex(gm, gn, ORDERS[order], out.ctypes.data), "sfc_tile_order")
+    return out[: gm * gn]
+
+
+def sfc_gemm_ws_size(M: int, N: int, K: int, ca_layers: int) -> int:
+    return int(lib.sfc_gemm_ws_size(M, N, K, ca_layers))
+
+
+def sfc_gemm_plan(M: int, N: int, K: int, ca_layers: int = 1, tile: str = "auto") -> dict:
+    plan = (ctypes.c_int64 * 7)()
+    _check(lib.sfc_gemm_plan(M, N, K, ca_layers, TILES[tile], plan), "sfc_gemm_plan")
+    keys = ["BM", "BN", "gm", "gn", "layers", "workgroups", "per_cu"]
+    return dict(zip(keys, [int(v) for v in plan]))
+
+
+def _matrix(t, name):
+    """(pointer, rows, cols, ld) of a 2-D torch tensor with unit column stride."""
+    if t.dim() != 2:
+        raise ValueError(f"{name} must be 2-D")
+    if t.shape[1] > 1 and t.stride(1) != 1:
+        raise ValueError(f"{name} must have unit column stride")
+    ld = t.stride(0) if t.shape[0] > 1 else max(t.shape[1], 1)
+    return t.data_ptr(), t.shape[0], t.shape[1], ld
+
+
+def _stream_handle(stream) -> Optional[int]:
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream
+
+
+def sfc_gemm_ex(A, B, C, ca_layers: int = 1, tile: str = "auto", order: str = "hilbert",
+                sched: str = "interleaved", workspace=None, stream=None) -> None:
+    """C = A @ B on the GPU.  A: (M, K) bf16, B: (K, N) bf16, C: (M, N) float32
+    or bfloat16 (the output type), all CUDA tensors with unit column stride."""
+    import torch
+    pa, M, K, lda = _matrix(A, "A")
+    pb, K2, N, ldb = _matrix(B, "B")
+    pc, M2, N2, ldc = _matrix(C, "C")
+    if K2 != K or M2 != M or N2 != N:
+        raise ValueError(f"shape mismatch: A {tuple(A.shape)} B {tuple(B.shape)} C {tuple(C.shape)}")
+    for t, n in ((A, "A"), (B, "B")):
+        if t.dtype not in (torch.bfloat16, torch.int16, torch.uint16):
+            raise TypeError(f"{n} must hold bf16 patterns")
+    if C.dtype == torch.float32:
+        out = SFC_OUT_F32
+    elif C.dtype == torch.bfloat16:
+        out = SFC_OUT_BF16
+    else:
+        raise TypeError("C must be float32 or bfloat16")
+    ws_ptr, ws_bytes = (None, 0) if workspace is None else (workspace.data_ptr(),
+                                                            workspace.numel() * workspace.element_size())
+    _check(lib.sfc_gemm_ex(M, N, K, pa, lda, pb, ldb, pc, ldc, out, ca_layers, TILES[tile],
+                           ORDERS[order], SCHEDS[sched], ws_ptr, ws_bytes, _stream_handle(stream)),
+           "sfc_gemm_ex")
+
+
+def sfc_gemm(A, B, C, ca_layers: int = 1, stream=None) -> None:
+    """C (float32) = A @ B with the default tile choice, curve order and schedule."""
+    pa, M, K, lda = _matrix(A, "A")
+    pb, _, N, ldb = _matrix(B, "B")
+    pc, _, _, ldc = _matrix(C, "C")
+    _check(lib.sfc_gemm(M, N, K, pa, lda, pb, ldb, pc, ldc, ca_layers, _stream_handle(stream)), "sfc_gemm")
+
+
+def sfc_gemm_bf16out(A, B, C, ca_layers: int = 1, stream=None) -> None:
+    """C (bfloat16) = A @ B with the default tile choice, curve order and schedule."""
+    pa, M, K, lda = _matrix(A, "A")
+    pb, _, N, ldb = _matrix(B, "B")
+    pc, _, _, ldc = _matrix(C, "C")
+    _check(lib.sfc_gemm_bf16out(M, N, K, pa, lda, pb, ldb, pc, ldc, ca_layers, _stream_handle(stream)),
+           "sfc_gemm_bf16out")
+
+
+def to_device_bf16(bits: np.ndarray, device="cuda"):
+    """Upload a uint16 array of bf16 patterns as a torch.bfloat16 CUDA tensor."""
+    import torch
+    t = torch.from_numpy(np.ascontiguousarray(bits).view(np.int16))
+    return t.to(device).view(torch.bfloat16)
