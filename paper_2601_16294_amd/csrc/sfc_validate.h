@@ -91,12 +91,14 @@ inline size_t ws_size(int64_t M, int64_t N, int64_t K, int ca_layers) {
   return (size_t)ce * (size_t)M * (size_t)N * 4u;
 }
 
-// 128-bit staging loads are legal when every row starts 16-byte aligned and
-// the K and N extents end on whole 8-element chunks.
+// 16-byte loads are legal when every row starts 16-byte aligned and the K and
+// N extents end on whole 8-element chunks.
 inline bool vector_loads_ok(const void* A, int64_t lda, const void* B, int64_t ldb, int64_t K,
                             int64_t N) {
+  // Per-lane byte offsets within a block are 32-bit: 256 rows of A, 64 of B.
   return ((uintptr_t)A % 16 == 0) && ((uintptr_t)B % 16 == 0) && (lda % 8 == 0) &&
-         (ldb % 8 == 0) && (K % 8 == 0) && (N % 8 == 0);
+         (ldb % 8 == 0) && (K % 8 == 0) && (N % 8 == 0) && lda < ((int64_t)1 << 20) &&
+         ldb < ((int64_t)1 << 22);
 }
 
 }  // namespace sfc
