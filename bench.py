@@ -51,6 +51,8 @@ def parse():
     ap.add_argument("--order", default="hilbert", choices=["hilbert", "row_major"])
     ap.add_argument("--sched", default="interleaved", choices=["interleaved", "block"])
     ap.add_argument("--only", default=None, help="run the kernel of one workload K times and exit")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="with --only: also run a plain device copy of MIB MiB (counter calibration)")
     return ap.parse_args()
 
 
@@ -98,12 +100,6 @@ def main():
         C = torch.empty((g.M, g.N), dtype=dtype, device=dev)
         return A, B, dA, dB, C
 
-    # ---------------------------------------------------------------- headline
-    w = W[HEADLINE]
-    g = w.gemms[0]
-    log(f"[bench] preparing {HEADLINE} {g.M}x{g.N}x{g.K}")
-    A_host, B_host, dA, dB, C = prepare(g)
-    plan = sg.sfc_gemm_plan(g.M, g.N, g.K, 1, w.tile)
     if args.only:
         ow = W[args.only]
         og = ow.gemms[0]
@@ -112,7 +108,21 @@ def main():
             run_once(oA, oB, oC, ow, ow.ca_layers[-1])
         torch.cuda.synchronize()
         log(f"[bench] ran {args.only} {args.steps} times")
+        if args.calibrate_copy:
+            n = args.calibrate_copy * 1024 * 1024 // 4
+            src = torch.ones(n, dtype=torch.float32, device=dev)
+            dst = torch.empty_like(src)
+            dst.copy_(src)
+            torch.cuda.synchronize()
+            log(f"[bench] copied {args.calibrate_copy} MiB")
         return
+
+    # ---------------------------------------------------------------- headline
+    w = W[HEADLINE]
+    g = w.gemms[0]
+    log(f"[bench] preparing {HEADLINE} {g.M}x{g.N}x{g.K}")
+    A_host, B_host, dA, dB, C = prepare(g)
+    plan = sg.sfc_gemm_plan(g.M, g.N, g.K, 1, w.tile)
     for _ in range(args.warmup):
         run_once(dA, dB, C, w, 1)
     torch.cuda.synchronize()
@@ -134,6 +144,17 @@ def main():
     log(f"[bench] headline {value:.1f} TFLOP/s (wall), kernel {kern_ms:.3f} ms -> {achieved:.1f} TFLOP/s")
     del dA, dB, C
     torch.cuda.empty_cache()
+
+    # ---------------------------------------------- sustained MFMA throughput
+    # Register-only MFMA loops: the clock the chip holds depends on how much the
+    # operand bits toggle, so the achievable ceiling for random data sits well
+    # below the published peak.
+    probe = {"random_operands": sg.sfc_probe_mfma(True, 400000),
+             "constant_operands": sg.sfc_probe_mfma(False, 400000)}
+    for v in probe.values():
+        v["tflops"] = round(v["tflops"], 1)
+        v["mhz"] = round(v["mhz"], 0)
+    log(f"[bench] MFMA probe {probe}")
 
     # --------------------------------------------------------------- workloads
     table = None
@@ -219,7 +240,9 @@ def main():
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                      "traffic": traffic_record(), "kernel": "sfc_gemm_kernel<256,256,bf16 out>",
-                     "kernel_ms": round(kern_ms, 4)},
+                     "kernel_ms": round(kern_ms, 4),
+                     "mfma_probe": probe,
+                     "frac_of_probe_random": round(achieved / probe["random_operands"]["tflops"], 4)},
         "cpu_baseline": cpu,
         "workloads": table,
     }

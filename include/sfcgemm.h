@@ -141,6 +141,21 @@ int sfc_gemm_ex(int64_t M, int64_t N, int64_t K,
  */
 int sfc_gemm_plan(int64_t M, int64_t N, int64_t K, int ca_layers, int tile, int64_t plan[7]);
 
+/*
+ * sfc_probe_mfma -- measurement aid for the roofline (the counterpart of the
+ * paper's compute micro-benchmark, Section III.B): register-only bf16 MFMA
+ * 32x32x16 throughput of the current device, 256 workgroups x 4 waves, each
+ * wave running `iterations` rounds of 16 independent MFMAs.
+ *   random_operands  1: operands drawn at random (they change between MFMAs, as
+ *                    in a GEMM); 0: constant operands.
+ *   tflops, mhz      out: achieved TFLOP/s and the mean shader clock sampled
+ *                    during the loop (MHz).  Host pointers.
+ * Synchronous (null stream); allocates and frees a 257 KiB device buffer.
+ * Returns SFC_OK, SFC_ERR_INVALID_ARG (iterations < 1, NULL outputs) or
+ * SFC_ERR_HIP.
+ */
+int sfc_probe_mfma(int random_operands, int iterations, double *tflops, double *mhz);
+
 /* Static text of a return code. */
 const char *sfc_strerror(int code);
 

@@ -19,7 +19,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libsfcgemm.so")
-SOURCES = ["sfc_order.hip", "sfc_gemm.hip", "sfc_reduce.hip", "sfcgemm_api.cpp"]
+SOURCES = ["sfc_order.hip", "sfc_gemm.hip", "sfc_reduce.hip", "sfc_probe.hip", "sfcgemm_api.cpp"]
 ARCH = "gfx950"
 
 
@@ -31,7 +31,7 @@ def hipcc() -> str:
 
 
 def common_flags():
-    return ["-x", "hip", f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
+    return ["-x", "hip", f"--offload-arch={ARCH}", "-O3", "-std=c++20", "-fPIC",
             "-ffp-contract=off",
             # keep the compiler from forming packed fp32 instructions
             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

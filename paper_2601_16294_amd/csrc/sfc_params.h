@@ -45,4 +45,8 @@ hipError_t gemm_occupancy(int tile, bool out_bf16, bool vec, int* blocks_per_cu)
 hipError_t launch_reduce(const float* W, int layers, int64_t M, int64_t N, void* C, int64_t ldc,
                          bool out_bf16, hipStream_t stream);
 
+// Register-only MFMA probe (256 workgroups x 4 waves); dev_out holds
+// 256*256 + 256 floats (the last 256: shader clock per workgroup in MHz).
+hipError_t run_mfma_probe(int random_operands, int iters, float* dev_out, double* ms);
+
 }  // namespace sfc

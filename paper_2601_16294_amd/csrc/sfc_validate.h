@@ -76,6 +76,9 @@ inline Checked check_gemm_args(int64_t M, int64_t N, int64_t K, const void* A, i
   if (ceil_div(M, 128) * ceil_div(N, 128) >= kMaxDim)
     return fail(SFC_ERR_UNSUPPORTED, "too many output blocks");
   const int ce = effective_layers(K, ca_layers, 64);
+  // task indices (blocks x layers) are 32-bit in the kernel
+  if (ceil_div(M, 128) * ceil_div(N, 128) * ce >= kMaxDim)
+    return fail(SFC_ERR_UNSUPPORTED, "too many output blocks x layers");
   if (ce > 1 && ws) {
     const uint64_t need = (uint64_t)ce * (uint64_t)M * (uint64_t)N * 4u;
     if (ws_bytes < need) return fail(SFC_ERR_WORKSPACE, "workspace smaller than sfc_gemm_ws_size()");

@@ -136,7 +136,8 @@ int make_plan(DeviceState& st, int64_t M, int64_t N, int64_t K, const void* A, i
   pl->gm = (int)sfc::ceil_div(M, pl->bm);
   pl->gn = (int)sfc::ceil_div(N, pl->bn);
   pl->nk = (int)(K > 0 ? sfc::ceil_div(K, sfc::kBK) : 0);
-  pl->vec = K == 0 || sfc::vector_loads_ok(A, lda, B, ldb, K, N);
+  // the fast path needs at least one K block per task
+  pl->vec = K > 0 && sfc::vector_loads_ok(A, lda, B, ldb, K, N);
   // layer copies are fp32 whatever the output type
   const bool kernel_bf16 = ob && pl->ce == 1;
   int rc = get_occupancy(st, pl->tile, kernel_bf16, pl->vec, &pl->occ);
@@ -273,6 +274,26 @@ int sfc_gemm_bf16out(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda
                      int64_t ldb, void* C, int64_t ldc, int ca_layers, void* stream) {
   return gemm_impl(M, N, K, A, lda, B, ldb, C, ldc, SFC_OUT_BF16, ca_layers, SFC_TILE_AUTO,
                    SFC_ORDER_HILBERT, SFC_SCHED_INTERLEAVED, nullptr, 0, stream);
+}
+
+int sfc_probe_mfma(int random_operands, int iterations, double* tflops, double* mhz) {
+  if (iterations < 1 || !tflops || !mhz) return set_error(SFC_ERR_INVALID_ARG, "invalid probe arguments");
+  const size_t n = 256 * 256 + 256;
+  float* d = nullptr;
+  hipError_t e = hipMalloc(&d, n * sizeof(float));
+  if (e != hipSuccess) return hip_fail(e, "hipMalloc(probe)");
+  double ms = 0.0;
+  e = sfc::run_mfma_probe(random_operands ? 1 : 0, iterations, d, &ms);
+  float clk[256];
+  if (e == hipSuccess) e = hipMemcpy(clk, d + 256 * 256, sizeof clk, hipMemcpyDeviceToHost);
+  (void)hipFree(d);
+  if (e != hipSuccess) return hip_fail(e, "MFMA probe");
+  double sum = 0.0;
+  for (int i = 0; i < 256; ++i) sum += clk[i];
+  *mhz = sum / 256.0;
+  const double flops = 256.0 * 4.0 * (double)iterations * 16.0 * (2.0 * 32 * 32 * 16);
+  *tflops = ms > 0.0 ? flops / (ms * 1e-3) / 1e12 : 0.0;
+  return SFC_OK;
 }
 
 int sfc_gemm_plan(int64_t M, int64_t N, int64_t K, int ca_layers, int tile, int64_t plan[7]) {

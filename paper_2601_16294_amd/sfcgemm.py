@@ -32,7 +32,8 @@ SCHEDS = {"interleaved": 0, "block": 1}
 
 # Every symbol include/sfcgemm.h declares.
 EXPORTS = ["sfc_tile_order", "sfc_tile_order_ex", "sfc_gemm", "sfc_gemm_bf16out", "sfc_gemm_ws_size",
-           "sfc_gemm_ex", "sfc_gemm_plan", "sfc_strerror", "sfc_last_error", "sfc_version"]
+           "sfc_gemm_ex", "sfc_gemm_plan", "sfc_probe_mfma", "sfc_strerror", "sfc_last_error",
+           "sfc_version"]
 
 
 class SfcError(RuntimeError):
@@ -61,6 +62,8 @@ def _load() -> ctypes.CDLL:
     lib.sfc_gemm_ws_size.restype = sz
     lib.sfc_gemm_plan.argtypes = [i64, i64, i64, i32, i32, ctypes.POINTER(ctypes.c_int64)]
     lib.sfc_gemm_plan.restype = i32
+    lib.sfc_probe_mfma.argtypes = [i32, i32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]
+    lib.sfc_probe_mfma.restype = i32
     lib.sfc_strerror.argtypes = [i32]
     lib.sfc_strerror.restype = ctypes.c_char_p
     lib.sfc_last_error.argtypes = []
@@ -102,6 +105,14 @@ def sfc_gemm_plan(M: int, N: int, K: int, ca_layers: int = 1, tile: str = "auto"
     _check(lib.sfc_gemm_plan(M, N, K, ca_layers, TILES[tile], plan), "sfc_gemm_plan")
     keys = ["BM", "BN", "gm", "gn", "layers", "workgroups", "per_cu"]
     return dict(zip(keys, [int(v) for v in plan]))
+
+
+def sfc_probe_mfma(random_operands: bool = True, iterations: int = 20000) -> dict:
+    """Register-only MFMA throughput and the shader clock during it."""
+    tf, mhz = ctypes.c_double(), ctypes.c_double()
+    _check(lib.sfc_probe_mfma(1 if random_operands else 0, iterations, ctypes.byref(tf), ctypes.byref(mhz)),
+           "sfc_probe_mfma")
+    return {"tflops": tf.value, "mhz": mhz.value}
 
 
 def _matrix(t, name):

@@ -110,3 +110,9 @@ def test_plan_validation(sg):
     plan = (ctypes.c_int64 * 7)()
     assert sg.lib.sfc_gemm_plan(0, 4, 4, 1, 0, plan) == -1
     assert sg.lib.sfc_gemm_plan(4, 4, 4, 1, 0, None) == -1
+
+
+def test_probe_validation(sg):
+    d = ctypes.c_double()
+    assert sg.lib.sfc_probe_mfma(1, 0, ctypes.byref(d), ctypes.byref(d)) == -1
+    assert sg.lib.sfc_probe_mfma(1, 10, None, ctypes.byref(d)) == -1

@@ -192,3 +192,10 @@ def test_plan_reports_grid():
     p = sg().sfc_gemm_plan(1024, 1024, 65536, 4, "128x128")
     assert (p["gm"], p["gn"], p["layers"]) == (8, 8, 4)
     assert p["workgroups"] == 256
+
+
+def test_mfma_probe_runs():
+    r = sg().sfc_probe_mfma(True, 2000)
+    c = sg().sfc_probe_mfma(False, 2000)
+    for v in (r, c):
+        assert 100.0 < v["tflops"] < 3000.0 and 500.0 < v["mhz"] < 3000.0
