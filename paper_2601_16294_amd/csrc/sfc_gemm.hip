@@ -17,18 +17,21 @@
 //     the interleaved schedule the P tasks in flight are one contiguous curve
 //     segment whose XCD sub-segments are compact patches sharing A rows and B
 //     columns in that XCD's L2;
-//   * A and B K-blocks are staged through LDS, double buffered, with one
-//     barrier per K block.  On the fast path (16-byte aligned rows) they go
-//     straight from global memory into LDS with buffer loads (lanes outside
-//     the matrix read zeros), so no registers hold staged data; otherwise
-//     they are assembled element by element in registers.  A is kept
-//     row-major [BM][64]; B is kept as loaded,
-//     [64][BN], and the MFMA B operand is assembled with the transposing LDS
-//     read (ds_read_b64_tr_b16).  16-byte chunks are XOR-swizzled so that both
-//     the fragment reads and the staging writes are free of bank conflicts on
-//     the 64-bank LDS;
+//   * fast path (16-byte aligned rows): A and B go straight from global memory
+//     into LDS with buffer loads (lanes outside the matrix read zeros), A in a
+//     ring of three 64-deep block slots [BM][64], B in a ring of four 32-deep
+//     stage slots [32][BN], with one barrier per 64-deep block.  The loads of
+//     the blocks two ahead are spread one pair per few MFMAs over the steps,
+//     so the texture path never sees a burst;
+//   * general path (any alignment): elements assembled in registers, two
+//     64-deep LDS buffers;
+//   * the MFMA B operand is read from [k][n] with the transposing LDS read
+//     (ds_read_b64_tr_b16); 16-byte chunks are XOR-swizzled so that the
+//     fragment reads and the staging writes are free of bank conflicts on the
+//     64-bank LDS;
 //   * bf16 MFMA 32x32x16 with fp32 accumulation (Section III.A's BRGEMM role).
 #include <type_traits>
+#include <utility>
 
 #include "sfc_params.h"
 
@@ -52,13 +55,16 @@ __device__ __forceinline__ int xcd_rank(int b, int P) {
 }
 
 // ---- LDS layouts ---------------------------------------------------------------
-// A block: [BM rows][64 k] bf16 = 8 chunks of 16 B per row; chunk c of row r is
-// stored at chunk c ^ ((r >> 1) & 7).  Sixteen consecutive rows read at one
-// logical chunk then hit 16 distinct 16-byte bank groups.
+// A block: [BM rows][KW k] bf16, KW/8 chunks of 16 B per row, chunk c of row r
+// stored at c ^ swizzle(r).  KW = 64 (general path): c ^ ((r >> 1) & 7); KW =
+// 32 (ring slots): c ^ ((r >> 2) & 3).  Either way the 16 rows that one quarter
+// of a wave reads at one logical chunk land on 16 distinct 16-byte bank groups.
+template <int KW>
 __device__ __forceinline__ int a_off(int row, int chunk) {
-  return row * kBK + ((chunk ^ ((row >> 1) & 7)) << 3);
+  if constexpr (KW == 64) return row * 64 + ((chunk ^ ((row >> 1) & 7)) << 3);
+  else return row * 32 + ((chunk ^ ((row >> 2) & 3)) << 3);
 }
-// B block: [64 k][BN n] bf16; chunk c (8 columns) of row k is stored at chunk
+// B block: [K k][BN n] bf16 (K = 64 or 32); chunk c (8 columns) of row k is stored at chunk
 // c ^ ((k & 3) << 2).  The transposing read touches 4 rows x 4 chunks per
 // 32 lanes, which this spreads over all 16 bank groups.
 template <int BN>
@@ -90,31 +96,18 @@ __device__ __forceinline__ u32x4 load_chunk(const uint16_t* base, int64_t ld, in
 }
 
 // ---- direct global -> LDS loads (fast path) ----------------------------------------
-// buffer_load_dwordx4 ... lds: every lane fetches 16 bytes at (descriptor base +
-// its voffset) and the wave writes them to LDS at M0 + 16*lane.  A lane whose
-// voffset lies at or beyond the descriptor's num_records fetches zeros.  The
-// instruction is issued from inline assembly so that the compiler does not
-// serialise later LDS reads behind it; the kernel orders it explicitly with
-// s_waitcnt vmcnt and workgroup barriers.
+// buffer_load_dwordx4 ... offset:O lds: every lane fetches 16 bytes at (descriptor
+// base + its voffset + O) and the wave writes them to LDS at M0 + O + 16*lane.  A
+// lane whose voffset lies at or beyond the descriptor's num_records fetches
+// zeros.  The instruction is issued from inline assembly so that the compiler
+// does not serialise later LDS reads behind it; the kernel orders it explicitly
+// with s_waitcnt vmcnt and workgroup barriers.  Raw buffer descriptor: 48-bit
+// base, stride 0, num_records, word 3 = 0x00020000 on gfx9 parts.
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 constexpr int kOobOffset = 0x7FFFFFF0;   // num_records; a lane at this offset reads zeros
 
-__device__ __forceinline__ i32x4 make_rsrc(const void* base) {
-  const uint64_t a = reinterpret_cast<uint64_t>(base);
-  // raw buffer: 48-bit base, stride 0, num_records, word 3 = 0x00020000 on gfx9 parts
-  i32x4 r = {(int)(uint32_t)a, (int)((uint32_t)(a >> 32) & 0xFFFFu), kOobOffset, 0x00020000};
-  r[0] = __builtin_amdgcn_readfirstlane(r[0]);
-  r[1] = __builtin_amdgcn_readfirstlane(r[1]);
-  return r;
-}
-
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
-}
-
-__device__ __forceinline__ void dma16(i32x4 rsrc, uint32_t lds_byte_addr, int voffset) {
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
-               :: "s"(lds_byte_addr), "v"(voffset), "s"(rsrc) : "memory");
 }
 
 template <int N>
@@ -135,40 +128,51 @@ struct Tile {
 };
 
 template <int BM, int BN>
+using Acc = f32x16[Tile<BM, BN>::FM][Tile<BM, BN>::FN];
+
+template <int BM, int BN>
 struct Frags {
   bf16x8 a[Tile<BM, BN>::FM];
   bf16x8 b[Tile<BM, BN>::FN];
 };
 
-// Operand fragments of k sub-step ks (16 deep) for this lane.
+// A operand fragment i of k sub-step ks (16 deep): lane holds row lane%32,
+// k = 8*(lane/32) .. +8.
+template <int BM, int BN, int KW>
+__device__ __forceinline__ void read_a(const uint16_t* As, int wm, int lane, int ks, int i,
+                                       Frags<BM, BN>& f) {
+  using T = Tile<BM, BN>;
+  const int row = wm * T::WTM + i * 32 + (lane & 31);
+  const int c = ks * 2 + (lane >> 5);
+  f.a[i] = *reinterpret_cast<const bf16x8*>(As + a_off<KW>(row, c));
+}
+// B operand fragment j: lane holds column lane%32, k = 8*(lane/32) .. +8.  Lane
+// (g = lane/16, jj = lane%16) points at row k, columns n..n+3; the transposing
+// read returns column n0 + jj of rows k0..k0+3 to lane jj.
 template <int BM, int BN>
+__device__ __forceinline__ void read_b(const uint16_t* Bs, int wn, int lane, int ks, int j,
+                                       Frags<BM, BN>& f) {
+  using T = Tile<BM, BN>;
+  const int g = lane >> 4, jj = lane & 15;
+  const int n = wn * T::WTN + j * 32 + ((g & 1) << 4) + ((jj & 3) << 2);
+  const int k = ks * 16 + ((g >> 1) << 3) + (jj >> 2);
+  const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(Bs + b_off<BN>(k, n)));
+  const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(Bs + b_off<BN>(k + 4, n)));
+  const i16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  f.b[j] = __builtin_bit_cast(bf16x8, v);
+}
+// All operand fragments of k sub-step ks for this lane.
+template <int BM, int BN, int KW>
 __device__ __forceinline__ void load_frags(const uint16_t* As, const uint16_t* Bs, int wm, int wn,
                                            int lane, int ks, Frags<BM, BN>& f) {
   using T = Tile<BM, BN>;
 #pragma unroll
-  for (int i = 0; i < T::FM; ++i) {
-    // A operand: lane holds row lane%32, k = 8*(lane/32) .. +8
-    const int row = wm * T::WTM + i * 32 + (lane & 31);
-    const int c = ks * 2 + (lane >> 5);
-    f.a[i] = *reinterpret_cast<const bf16x8*>(As + a_off(row, c));
-  }
+  for (int i = 0; i < T::FM; ++i) read_a<BM, BN, KW>(As, wm, lane, ks, i, f);
 #pragma unroll
-  for (int j = 0; j < T::FN; ++j) {
-    // B operand: lane holds column lane%32, k = 8*(lane/32) .. +8.  Lane
-    // (g = lane/16, jj = lane%16) points at row k, columns n..n+3; the
-    // transposing read returns column n0 + jj of rows k0..k0+3 to lane jj.
-    const int g = lane >> 4, jj = lane & 15;
-    const int n = wn * T::WTN + j * 32 + ((g & 1) << 4) + ((jj & 3) << 2);
-    const int k = ks * 16 + ((g >> 1) << 3) + (jj >> 2);
-    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(Bs + b_off<BN>(k, n)));
-    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(Bs + b_off<BN>(k + 4, n)));
-    const i16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-    f.b[j] = __builtin_bit_cast(bf16x8, v);
-  }
+  for (int j = 0; j < T::FN; ++j) read_b<BM, BN>(Bs, wn, lane, ks, j, f);
 }
 
-// acc += one 16-deep step, with the fragment reads of the following step
-// interleaved between the MFMAs (one LDS read after each of the first MFMAs).
+// acc += one 16-deep step.
 template <int BM, int BN>
 __device__ __forceinline__ void mma_step(const Frags<BM, BN>& cur,
                                          f32x16 (&acc)[Tile<BM, BN>::FM][Tile<BM, BN>::FN]) {
@@ -182,112 +186,329 @@ __device__ __forceinline__ void mma_step(const Frags<BM, BN>& cur,
       acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cur.b[j], cur.a[i], acc[i][j], 0, 0, 0);
 }
 
+// ---- fast path: rings of LDS slots ---------------------------------------------------------
+// A is staged per 64-deep block, in three slots of [BM][64] (a_off<64>): a row of
+// a block is one full 128-byte line of A.  B is staged per 32-deep stage, in
+// four slots of [32][BN] (b_off).  Loads are buffer loads of 1 KiB (16 B per
+// lane) written straight into LDS.  Wave w loads A segments w*APB .. +APB-1
+// (8 rows each) of a block and B segments w*BPW .. +BPW-1 of a stage; a wave's
+// segments are consecutive KiB, so up to four share one M0 value and differ
+// only in the instruction offset, which the hardware adds to both the LDS
+// address and the memory address.  The per-lane voffset is biased by kBias -
+// offset and the descriptor base lowered by kBias to cancel the memory side.
+//
+// Every instruction of the loop counts: with one wave per SIMD a wave issues
+// at most one instruction per four clocks, and an MFMA 32x32x16 occupies the
+// matrix core for 32, so the loop keeps its other work (LDS reads, loads,
+// address arithmetic) to a few instructions per MFMA, spread evenly.
+constexpr int kSK = 32;        // K depth of one B stage
+constexpr int kASlots = 3;     // A block slots
+constexpr int kBSlots = 4;     // B stage slots
+constexpr int kBias = 4096;    // bytes; keeps every biased voffset positive
+
 template <int BM, int BN>
-__device__ __forceinline__ void interleave_reads_with_mfma() {
-  using T = Tile<BM, BN>;
-  constexpr int kMfma = T::FM * T::FN;
-  constexpr int kReads = T::FM + 2 * T::FN;
-  constexpr int kPaired = kReads < kMfma ? kReads : kMfma;
-#pragma unroll
-  for (int r = 0; r < kPaired; ++r) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
-    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one LDS read
-  }
-  if (kMfma > kPaired) __builtin_amdgcn_sched_group_barrier(0x008, kMfma - kPaired, 0);
-  if (kReads > kPaired) __builtin_amdgcn_sched_group_barrier(0x100, kReads - kPaired, 0);
+struct Ring {
+  static constexpr int A_BLK = BM * kBK;                 // elements of one A block
+  static constexpr int B_STG = kSK * BN;                 // elements of one B stage
+  static constexpr int A_BYTES = A_BLK * 2, B_BYTES = B_STG * 2;
+  static constexpr int B_OFF = kASlots * A_BYTES;        // byte offset of the B slots
+  static constexpr int APB = A_BYTES / 1024 / 4;         // A loads per wave per block
+  static constexpr int BPW = B_BYTES / 1024 / 4;         // B loads per wave per stage
+  static constexpr int ELEMS = kASlots * A_BLK + kBSlots * B_STG;
+  static_assert(APB % 4 == 0 && (BPW == 2 || BPW == 4), "tile shape");
+};
+
+// Two loads sharing M0: LDS M0+OFF+16*lane and M0+OFF+1024+16*lane.
+template <int OFF>
+__device__ __forceinline__ void dma16_pair(i32x4 rsrc, uint32_t m0_value, int v0, int v1) {
+  static_assert(OFF + 1024 <= 4095, "instruction offset range");
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\t"
+               "buffer_load_dwordx4 %1, %3, 0 offen offset:%4 lds\n\t"
+               "buffer_load_dwordx4 %2, %3, 0 offen offset:%5 lds"
+               :: "s"(m0_value), "v"(v0), "v"(v1), "s"(rsrc), "n"(OFF), "n"(OFF + 1024) : "memory");
 }
 
-// ---- main loop, fast path: buffer loads straight into LDS ---------------------------------
-// Wave w fills LDS 1 KiB segments w, w+4, w+8, ...; lane l of a segment holds
-// physical 16-byte chunk l of it, i.e. it loads the logical chunk that the
-// swizzle stores there.  Lanes outside M, N or K use an offset past the
-// buffer's range and write zeros.
-//
-// Software pipeline (two LDS buffers, one barrier per 64-deep block):
-//   step 0..2 of block kt: MFMAs of step s, reads of step s+1 from buffer b;
-//   step 3: wait for this wave's loads of block kt+1 and its reads of step 3,
-//           barrier (block kt+1 is now visible and buffer b is free), issue the
-//           loads of block kt+2 into b, then the MFMAs of step 3 with the reads
-//           of step 0 of block kt+1 from buffer b^1.
+__device__ __forceinline__ i32x4 make_rsrc_addr(uint64_t a) {
+  i32x4 r = {(int)(uint32_t)a, (int)((uint32_t)(a >> 32) & 0xFFFFu), kOobOffset, 0x00020000};
+  r[0] = __builtin_amdgcn_readfirstlane(r[0]);
+  r[1] = __builtin_amdgcn_readfirstlane(r[1]);
+  return r;
+}
+
+// Per-lane, per-task load offsets (bytes, biased).
 template <int BM, int BN>
-__device__ __forceinline__ void main_loop_direct(const GemmParams& p, uint16_t* smem, int64_t m0,
-                                                 int64_t n0, int kt0, int kt1, int wave, int lane,
-                                                 f32x16 (&acc)[Tile<BM, BN>::FM][Tile<BM, BN>::FN]) {
-  using T = Tile<BM, BN>;
-  constexpr int kStage = T::A_ELEMS + T::B_ELEMS;
-  constexpr int kLoads = T::A_CH + T::B_CH;
-  const int wm = wave >> 1, wn = wave & 1;
-  int a_voff[T::A_CH], a_k[T::A_CH], b_voff[T::B_CH], b_k[T::B_CH];
+struct RingLanes {
+  int a_voff[Ring<BM, BN>::APB];
+  int b_voff[Ring<BM, BN>::BPW];
+};
+
+// K index (within a block or stage) at which load j of this lane starts.
+__device__ __forceinline__ int a_load_k(int wave, int apb, int j, int lane) {
+  const int row = (wave * apb + j) * 8 + (lane >> 3);
+  return ((lane & 7) ^ ((row >> 1) & 7)) * 8;
+}
+template <int BN>
+__device__ __forceinline__ int b_load_k(int wave, int bpw, int j, int lane) {
+  return ((wave * bpw + j) * 512 + lane * 8) / BN;
+}
+
+template <int BM, int BN>
+__device__ __forceinline__ void ring_lanes(const GemmParams& p, int64_t m0, int64_t n0, int wave,
+                                           int lane, RingLanes<BM, BN>& L) {
+  using R = Ring<BM, BN>;
 #pragma unroll
-  for (int i = 0; i < T::A_CH; ++i) {
-    const int seg = i * 4 + wave;               // rows 8*seg .. 8*seg+7
-    const int row = seg * 8 + (lane >> 3);
+  for (int j = 0; j < R::APB; ++j) {
+    const int row = (wave * R::APB + j) * 8 + (lane >> 3);
     const int c = (lane & 7) ^ ((row >> 1) & 7);
-    a_k[i] = c * 8;
-    a_voff[i] = (m0 + row < p.M) ? (int)((row * p.lda + c * 8) * 2) : kOobOffset;
+    L.a_voff[j] = (m0 + row < p.M) ? (int)((row * p.lda + c * 8) * 2) + kBias - (j & 3) * 1024 : kOobOffset;
   }
 #pragma unroll
-  for (int i = 0; i < T::B_CH; ++i) {
-    const int seg = i * 4 + wave;
-    const int e = seg * 512 + lane * 8;         // element index in the [64][BN] block
+  for (int j = 0; j < R::BPW; ++j) {
+    const int e = (wave * R::BPW + j) * 512 + lane * 8;   // element index in the [32][BN] stage
     const int k = e / BN;
     const int c = ((e % BN) >> 3) ^ ((k & 3) << 2);
-    b_k[i] = k;
-    b_voff[i] = (n0 + c * 8 < p.N) ? (int)((k * p.ldb + c * 8) * 2) : kOobOffset;
+    L.b_voff[j] = (n0 + c * 8 < p.N) ? (int)((k * p.ldb + c * 8) * 2) + kBias - j * 1024 : kOobOffset;
   }
-  const uint32_t smem_lds = lds_addr(smem);
-  auto issue = [&](int kt, int buf) {
-    const int64_t k0 = (int64_t)kt * kBK;
-    const i32x4 ra = make_rsrc(p.A + m0 * p.lda + k0);
-    const i32x4 rb = make_rsrc(p.B + k0 * p.ldb + n0);
-    const uint32_t a_base = smem_lds + (uint32_t)(buf * kStage) * 2u;
-    const uint32_t b_base = a_base + (uint32_t)T::A_ELEMS * 2u;
-#pragma unroll
-    for (int i = 0; i < T::A_CH; ++i)
-      dma16(ra, a_base + (uint32_t)((i * 4 + wave) * 1024),
-            (k0 + a_k[i] < p.K) ? a_voff[i] : kOobOffset);
-#pragma unroll
-    for (int i = 0; i < T::B_CH; ++i)
-      dma16(rb, b_base + (uint32_t)((i * 4 + wave) * 1024),
-            (k0 + b_k[i] < p.K) ? b_voff[i] : kOobOffset);
-  };
+}
 
-  issue(kt0, 0);
-  if (kt0 + 1 < kt1) {
-    issue(kt0 + 1, 1);
-    wait_vmem_at_most<kLoads>();
+// Per-lane LDS byte offsets of the fragment reads within a slot: A fragment i
+// of 16-deep sub-step ka (0..3 within a block) at a_rd[ka] + i*4096 (the
+// swizzle does not depend on i); the two halves of B fragment j of sub-step ks
+// (0..1 within a stage) at b_rd[ks][j] and b_rd[ks][j] + 8*BN.
+template <int BM, int BN>
+struct ReadOffsets {
+  uint32_t a_rd[4];
+  uint32_t b_rd[2][Tile<BM, BN>::FN];
+};
+
+template <int BM, int BN>
+__device__ __forceinline__ void read_offsets(int wm, int wn, int lane, ReadOffsets<BM, BN>& o) {
+  using T = Tile<BM, BN>;
+  const int row = wm * T::WTM + (lane & 31);
+#pragma unroll
+  for (int ka = 0; ka < 4; ++ka) o.a_rd[ka] = (uint32_t)(a_off<64>(row, ka * 2 + (lane >> 5)) * 2);
+  const int g = lane >> 4, jj = lane & 15;
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks) {
+    const int k = ks * 16 + ((g >> 1) << 3) + (jj >> 2);
+#pragma unroll
+    for (int j = 0; j < T::FN; ++j) {
+      const int n = wn * T::WTN + j * 32 + ((g & 1) << 4) + ((jj & 3) << 2);
+      o.b_rd[ks][j] = (uint32_t)(b_off<BN>(k, n) * 2);
+    }
+  }
+}
+
+typedef __attribute__((address_space(3))) const bf16x8 lds_bf16x8;
+
+// Read item t of a step, in the order the next step's MFMAs consume them:
+// A0, B0, B1, .., B(FN-1), A1, .., A(FM-1).
+template <int BM, int BN>
+__device__ __forceinline__ void read_item(int t, uint32_t a_base, const uint32_t* b_base, Frags<BM, BN>& f) {
+  using T = Tile<BM, BN>;
+  if (t == 0 || t > T::FN) {
+    const int i = t == 0 ? 0 : t - T::FN;
+    f.a[i] = *(lds_bf16x8*)(uintptr_t)(a_base + (uint32_t)(i * 4096));
+  } else {
+    const int j = t - 1;
+    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(uintptr_t)b_base[j]);
+    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(uintptr_t)(b_base[j] + 8 * BN));
+    const i16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    f.b[j] = __builtin_bit_cast(bf16x8, v);
+  }
+}
+
+// Loads of one A block or one B stage: descriptor and M0 of this wave's first segment.
+struct SlotDma {
+  i32x4 rsrc;
+  uint32_t m0;
+};
+
+// Load pair q (loads 2q, 2q+1) of an A block (OP 1) or a B stage (OP 2).
+template <int BM, int BN, int OP, int Q>
+__device__ __forceinline__ void dma_pair(const SlotDma& d, const RingLanes<BM, BN>& L) {
+  constexpr int j = 2 * Q;
+  if constexpr (OP == 1)
+    dma16_pair<(j & 3) * 1024>(d.rsrc, d.m0 + (uint32_t)((j >> 2) * 4096), L.a_voff[j], L.a_voff[j + 1]);
+  else
+    dma16_pair<j * 1024>(d.rsrc, d.m0, L.b_voff[j], L.b_voff[j + 1]);
+}
+
+// All loads of an A block (OP 1) or a B stage (OP 2).
+template <int BM, int BN, int OP>
+__device__ __forceinline__ void dma_all(const SlotDma& d, const RingLanes<BM, BN>& L) {
+  using R = Ring<BM, BN>;
+  [&]<int... q>(std::integer_sequence<int, q...>) {
+    (dma_pair<BM, BN, OP, q>(d, L), ...);
+  }(std::make_integer_sequence<int, (OP == 1 ? R::APB : R::BPW) / 2>{});
+}
+
+// Turn the lanes whose load starts at a K index >= kin (within the block or
+// stage) into out-of-range lanes, for the loads of a block that runs past K.
+// Applied once more with a smaller kin it only masks further.
+template <int BM, int BN, bool A, bool B>
+__device__ __forceinline__ void mask_lanes(RingLanes<BM, BN>& L, int wave, int lane, int64_t kin) {
+  using R = Ring<BM, BN>;
+  if constexpr (A) {
+#pragma unroll
+    for (int j = 0; j < R::APB; ++j)
+      if (a_load_k(wave, R::APB, j, lane) >= kin) L.a_voff[j] = kOobOffset;
+  }
+  if constexpr (B) {
+#pragma unroll
+    for (int j = 0; j < R::BPW; ++j)
+      if (b_load_k<BN>(wave, R::BPW, j, lane) >= kin) L.b_voff[j] = kOobOffset;
+  }
+}
+
+// One 16-deep step with a fixed instruction order: group g issues MFMA g of
+// `cur` (i-major), then the fragment reads of `nxt` that fall on g, then the
+// load pair that falls on g.  Loads: pairs [Q0, Q1) of an A block (OP 1) or
+// of a B stage (OP 2), spread evenly over the groups so that neither the LDS
+// nor the texture path receives a burst.
+template <int BM, int BN, int OP, int Q0, int Q1>
+__device__ __forceinline__ void ring_step(Acc<BM, BN>& acc, const Frags<BM, BN>& cur, Frags<BM, BN>& nxt,
+                                          uint32_t a_base, uint32_t b_slot, int ks,
+                                          const ReadOffsets<BM, BN>& o, bool dma_on, const SlotDma& d,
+                                          const RingLanes<BM, BN>& L) {
+  using T = Tile<BM, BN>;
+  constexpr int G = T::FM * T::FN;
+  constexpr int NI = T::FM + T::FN;
+  constexpr int NP = Q1 - Q0;
+  uint32_t b_base[T::FN];
+#pragma unroll
+  for (int j = 0; j < T::FN; ++j) b_base[j] = b_slot + o.b_rd[ks][j];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    const int i = g / T::FN, j = g % T::FN;
+    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cur.b[j], cur.a[i], acc[i][j], 0, 0, 0);
+#pragma unroll
+    for (int t = 0; t < NI; ++t)
+      if ((t * G) / NI == g) read_item<BM, BN>(t, a_base, b_base, nxt);
+    if constexpr (NP > 0) {
+      if (dma_on) {
+        [&]<int... q>(std::integer_sequence<int, q...>) {
+          ((void)(((2 * q + 1) * G) / (2 * NP) == g ? (dma_pair<BM, BN, OP, Q0 + q>(d, L), 0) : 0), ...);
+        }(std::make_integer_sequence<int, NP>{});
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
+// Where the blocks and stages of one task come from and go to.
+template <int BM, int BN>
+struct RingAddr {
+  uint64_t a0, b0;           // byte address of the first block's A origin and B origin, minus kBias
+  uint64_t b_step;           // bytes between consecutive B stages (32 rows of B)
+  uint32_t lds0;             // LDS byte address of the ring
+  int wave;
+  // A block kb: descriptor and this wave's M0 in A slot kb mod 3
+  __device__ __forceinline__ SlotDma a_blk(int kb) const {
+    using R = Ring<BM, BN>;
+    SlotDma d;
+    d.rsrc = make_rsrc_addr(a0 + (uint64_t)kb * (kBK * 2));
+    d.m0 = lds0 + (uint32_t)((kb % kASlots) * R::A_BYTES + wave * R::APB * 1024);
+    return d;
+  }
+  // B stage x: descriptor and this wave's M0 in B slot x mod 4
+  __device__ __forceinline__ SlotDma b_stg(int x) const {
+    using R = Ring<BM, BN>;
+    SlotDma d;
+    d.rsrc = make_rsrc_addr(b0 + (uint64_t)x * b_step);
+    d.m0 = lds0 + (uint32_t)(R::B_OFF + (x & (kBSlots - 1)) * R::B_BYTES + wave * R::BPW * 1024);
+    return d;
+  }
+  // LDS byte addresses of the slots, materialised as scalars so that the
+  // fragment reads add them once per base address and fold the rest into
+  // their immediate offsets
+  __device__ __forceinline__ uint32_t a_slot(int kb) const {
+    return (uint32_t)__builtin_amdgcn_readfirstlane((int)(lds0 + (uint32_t)((kb % kASlots) * Ring<BM, BN>::A_BYTES)));
+  }
+  __device__ __forceinline__ uint32_t b_slot(int x) const {
+    using R = Ring<BM, BN>;
+    return (uint32_t)__builtin_amdgcn_readfirstlane((int)(lds0 + (uint32_t)(R::B_OFF + (x & (kBSlots - 1)) * R::B_BYTES)));
+  }
+};
+
+// The K loop of one task over nb 64-deep blocks.  Block b = A block b and B
+// stages x0 = 2b, x0+1; its 16-deep steps are A (x0/ks0), B (x0/ks1), C
+// (x0+1/ks0), D (x0+1/ks1).  Each step runs the MFMAs of one sub-step while it
+// reads the operands of the next:
+//   step A: reads A b/1, B x0/1;    loads: B stage x0+3
+//   step B: reads A b/2, B x0+1/0;  loads: first half of A block b+2
+//   step C: reads A b/3, B x0+1/1;  loads: second half of A block b+2
+//   wait until A block b+1 and B stages <= x0+3 have landed (A block b+2 may
+//   still be in flight), barrier b
+//   step D: reads A b+1/0, B x0+2/0; loads: B stage x0+4
+// A block kb lives in A slot kb mod 3, B stage x in B slot x mod 4.  Every load
+// goes into a slot whose last reads were issued before the barrier that
+// precedes the load; the shortest lead from a load to the barrier that
+// publishes it is two steps.
+//
+// When the last block runs past K (kin_last < 64), its loads are the last ones
+// issued, in the order A block nb-1, B stage 2nb-2, B stage 2nb-1: the lanes
+// are masked at kin_last right before the first of them, and B once more at
+// kin_last - 32 before the last.
+template <int BM, int BN>
+__device__ __forceinline__ void main_loop_ring(const RingAddr<BM, BN>& ra, int nb, int64_t kin_last,
+                                               const ReadOffsets<BM, BN>& o, RingLanes<BM, BN>& L, int lane,
+                                               Acc<BM, BN>& acc) {
+  using R = Ring<BM, BN>;
+  constexpr int AH = R::APB / 4;      // load pairs per half A block
+  constexpr int BQ = R::BPW / 2;      // load pairs per B stage
+  const int wave = ra.wave;
+  const int nst = 2 * nb;
+  const bool masked = kin_last < kBK;
+
+  // prologue: A block 0, B stages 0 and 1, then A block 1 and B stage 2
+  if (masked && nb == 1) mask_lanes<BM, BN, true, true>(L, wave, lane, kin_last);
+  dma_all<BM, BN, 1>(ra.a_blk(0), L);
+  dma_all<BM, BN, 2>(ra.b_stg(0), L);
+  if (masked && nb == 1) mask_lanes<BM, BN, false, true>(L, wave, lane, kin_last - kSK);
+  dma_all<BM, BN, 2>(ra.b_stg(1), L);
+  if (nb > 1) {
+    if (masked && nb == 2) mask_lanes<BM, BN, true, true>(L, wave, lane, kin_last);
+    dma_all<BM, BN, 1>(ra.a_blk(1), L);
+    dma_all<BM, BN, 2>(ra.b_stg(2), L);
+    wait_vmem_at_most<R::APB + R::BPW>();
   } else {
     wait_vmem_at_most<0>();
   }
   __syncthreads();
 
   Frags<BM, BN> f0, f1;
-  load_frags<BM, BN>(smem, smem + T::A_ELEMS, wm, wn, lane, 0, f0);
-  for (int kt = kt0; kt < kt1; ++kt) {
-    const int buf = (kt - kt0) & 1;
-    const uint16_t* As = smem + buf * kStage;
-    const uint16_t* Bs = As + T::A_ELEMS;
-    load_frags<BM, BN>(As, Bs, wm, wn, lane, 1, f1);
-    mma_step<BM, BN>(f0, acc);
-    interleave_reads_with_mfma<BM, BN>();
-    load_frags<BM, BN>(As, Bs, wm, wn, lane, 2, f0);
-    mma_step<BM, BN>(f1, acc);
-    interleave_reads_with_mfma<BM, BN>();
-    load_frags<BM, BN>(As, Bs, wm, wn, lane, 3, f1);
-    mma_step<BM, BN>(f0, acc);
-    interleave_reads_with_mfma<BM, BN>();
-    // Step 3 runs the same way on the last block (one MFMA chain, no copies
-    // of the accumulators); the reads of the other buffer are then unused.
-    wait_vmem_at_most<0>();
+  {
+    uint32_t b_base[Tile<BM, BN>::FN];
+    const uint32_t bs = ra.b_slot(0);
+#pragma unroll
+    for (int j = 0; j < Tile<BM, BN>::FN; ++j) b_base[j] = bs + o.b_rd[0][j];
+    const uint32_t as = ra.a_slot(0) + o.a_rd[0];
+#pragma unroll
+    for (int t = 0; t < Tile<BM, BN>::FM + Tile<BM, BN>::FN; ++t) read_item<BM, BN>(t, as, b_base, f0);
+  }
+  for (int b = 0; b < nb; ++b) {
+    const int x0 = 2 * b;
+    const uint32_t as = ra.a_slot(b);
+    if (masked && b == nb - 2) mask_lanes<BM, BN, false, true>(L, wave, lane, kin_last - kSK);
+    ring_step<BM, BN, 2, 0, BQ>(acc, f0, f1, as + o.a_rd[1], ra.b_slot(x0), 1, o, x0 + 3 < nst,
+                                ra.b_stg(x0 + 3), L);
+    if (masked && b == nb - 3) mask_lanes<BM, BN, true, true>(L, wave, lane, kin_last);
+    {
+      const SlotDma d = ra.a_blk(b + 2);
+      const bool on = b + 2 < nb;
+      const uint32_t bs = ra.b_slot(x0 + 1);
+      ring_step<BM, BN, 1, 0, AH>(acc, f1, f0, as + o.a_rd[2], bs, 0, o, on, d, L);
+      ring_step<BM, BN, 1, AH, 2 * AH>(acc, f0, f1, as + o.a_rd[3], bs, 1, o, on, d, L);
+      if (on) wait_vmem_at_most<R::APB>();
+      else wait_vmem_at_most<0>();
+    }
     wait_lds_all();
     __syncthreads();
-    if (kt + 2 < kt1) issue(kt + 2, buf);
-    const uint16_t* An = smem + (buf ^ 1) * kStage;
-    load_frags<BM, BN>(An, An + T::A_ELEMS, wm, wn, lane, 0, f0);
-    mma_step<BM, BN>(f1, acc);
-    interleave_reads_with_mfma<BM, BN>();
+    ring_step<BM, BN, 2, 0, BQ>(acc, f1, f0, ra.a_slot(b + 1) + o.a_rd[0], ra.b_slot(x0 + 2), 0, o,
+                                x0 + 4 < nst, ra.b_stg(x0 + 4), L);
   }
-  // the next task's first loads overwrite both buffers
+  // the ring's next user starts with a fresh prologue
   wait_lds_all();
   __syncthreads();
 }
@@ -320,7 +541,7 @@ __device__ __forceinline__ void main_loop_staged(const GemmParams& p, uint16_t* 
 #pragma unroll
     for (int i = 0; i < T::A_CH; ++i) {
       const int q = tid + kThreads * i;
-      *reinterpret_cast<u32x4*>(As + a_off(q >> 3, q & 7)) = ra[i];
+      *reinterpret_cast<u32x4*>(As + a_off<64>(q >> 3, q & 7)) = ra[i];
     }
 #pragma unroll
     for (int i = 0; i < T::B_CH; ++i) {
@@ -339,7 +560,7 @@ __device__ __forceinline__ void main_loop_staged(const GemmParams& p, uint16_t* 
 #pragma unroll
     for (int ks = 0; ks < kBK / 16; ++ks) {
       Frags<BM, BN> f;
-      load_frags<BM, BN>(As, As + T::A_ELEMS, wm, wn, lane, ks, f);
+      load_frags<BM, BN, 64>(As, As + T::A_ELEMS, wm, wn, lane, ks, f);
       mma_step<BM, BN>(f, acc);
     }
     if (more) store_blocks(buf ^ 1);
@@ -408,12 +629,16 @@ template <int BM, int BN, bool OUT_BF16, bool VEC>
 __global__ __launch_bounds__(kThreads, 1) void sfc_gemm_kernel(GemmParams p) {
   using T = Tile<BM, BN>;
   static_assert(T::A_CH >= 1 && T::B_CH >= 1, "tile too small for 256 threads");
-  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * (T::A_ELEMS + T::B_ELEMS)];
+  // fast path: the ring of stage slots; general path: two 64-deep blocks
+  constexpr int kSmem = VEC ? Ring<BM, BN>::ELEMS : 2 * (T::A_ELEMS + T::B_ELEMS);
+  __shared__ __attribute__((aligned(16))) uint16_t smem[kSmem];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
+  ReadOffsets<BM, BN> ro;
+  if constexpr (VEC) read_offsets<BM, BN>(wm, wn, lane, ro);
 
   const int P = gridDim.x;
   const int rank = xcd_rank(blockIdx.x, P);
@@ -452,8 +677,21 @@ __global__ __launch_bounds__(kThreads, 1) void sfc_gemm_kernel(GemmParams p) {
         for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
     if (kt0 < kt1) {
-      if constexpr (VEC) main_loop_direct<BM, BN>(p, smem, m0, n0, kt0, kt1, wave, lane, acc);
-      else main_loop_staged<BM, BN>(p, smem, m0, n0, kt0, kt1, tid, acc);
+      if constexpr (VEC) {
+        // a last block that runs past K is loaded with per-lane masks
+        const int64_t kin_last = p.K - (int64_t)(kt1 - 1) * kBK;
+        RingLanes<BM, BN> L;
+        ring_lanes<BM, BN>(p, m0, n0, wave, lane, L);
+        RingAddr<BM, BN> ra;
+        ra.a0 = reinterpret_cast<uint64_t>(p.A + m0 * p.lda + (int64_t)kt0 * kBK) - kBias;
+        ra.b0 = reinterpret_cast<uint64_t>(p.B + (int64_t)kt0 * kBK * p.ldb + n0) - kBias;
+        ra.b_step = (uint64_t)kSK * (uint64_t)p.ldb * 2;
+        ra.lds0 = lds_addr(smem);
+        ra.wave = wave;
+        main_loop_ring<BM, BN>(ra, kt1 - kt0, kin_last, ro, L, lane, acc);
+      } else {
+        main_loop_staged<BM, BN>(p, smem, m0, n0, kt0, kt1, tid, acc);
+      }
     }
 
     // Epilogue.  Accumulator element e of fragment (i, j) is row lane%32 and

@@ -100,26 +100,30 @@ int tile_from_api(int t) {
   }
 }
 
-// Block shape for SFC_TILE_AUTO: the shape with the smallest estimated time,
-// estimated as (rounds of tasks over the persistent slots) x (block area per
-// unit of throughput).  Larger blocks reuse more data per LDS byte and sustain
-// a higher MFMA rate; the relative rates below are per-block throughputs.
-int choose_tile(int64_t M, int64_t N, int ce, int num_cus) {
-  static const int order[4] = {sfc::kT256x256, sfc::kT256x128, sfc::kT128x256, sfc::kT128x128};
-  static const double rate[4] = {1.0, 0.9, 0.9, 0.75};
-  static const int slots_per_cu[4] = {1, 1, 1, 2};
-  int best = sfc::kT128x128;
+// Block shape for SFC_TILE_AUTO: the shape with the smallest estimated time.
+// A CU runs `occ` workgroups at once and completes a BM x BN block at a rate
+// proportional to rate[] (measured on MI355X with the 8192^3 bf16 GEMM, where
+// every shape fills whole rounds); the persistent grid takes ceil(tasks /
+// (CUs * occ)) rounds, each costing occ * BM * BN / rate.  Ties keep the
+// earlier shape.
+int choose_tile(DeviceState& st, int64_t M, int64_t N, int ce, bool ob, bool vec, int* tile) {
+  static const int order[4] = {sfc::kT256x256, sfc::kT128x256, sfc::kT256x128, sfc::kT128x128};
+  static const double rate[4] = {1.0, 0.93, 0.93, 0.67};
+  int best = sfc::kT256x256;
   double best_t = 1e300;
   for (int i = 0; i < 4; ++i) {
     const int t = order[i];
+    int occ = 1;
+    const int rc = get_occupancy(st, t, ob && ce == 1, vec, &occ);
+    if (rc != SFC_OK) return rc;
     const int64_t bm = sfc::tile_bm(t), bn = sfc::tile_bn(t);
     const int64_t tasks = sfc::ceil_div(M, bm) * sfc::ceil_div(N, bn) * ce;
-    const int64_t slots = (int64_t)num_cus * slots_per_cu[i];
-    const int64_t rounds = sfc::ceil_div(tasks, slots);
-    const double est = (double)rounds * (double)(bm * bn) / rate[i] / slots_per_cu[i];
+    const int64_t rounds = sfc::ceil_div(tasks, (int64_t)st.num_cus * occ);
+    const double est = (double)rounds * (double)occ * (double)(bm * bn) / rate[i];
     if (est < best_t * 0.999) { best_t = est; best = t; }
   }
-  return best;
+  *tile = best;
+  return SFC_OK;
 }
 
 struct Plan {
@@ -130,17 +134,23 @@ struct Plan {
 int make_plan(DeviceState& st, int64_t M, int64_t N, int64_t K, const void* A, int64_t lda,
               const void* B, int64_t ldb, bool ob, int ca_layers, int tile_api, Plan* pl) {
   pl->ce = sfc::effective_layers(K, ca_layers, sfc::kBK);
-  pl->tile = tile_api == SFC_TILE_AUTO ? choose_tile(M, N, pl->ce, st.num_cus) : tile_from_api(tile_api);
+  // the fast path needs at least one K block per task
+  pl->vec = K > 0 && sfc::vector_loads_ok(A, lda, B, ldb, K, N);
+  int rc = SFC_OK;
+  if (tile_api == SFC_TILE_AUTO) {
+    rc = choose_tile(st, M, N, pl->ce, ob, pl->vec, &pl->tile);
+    if (rc != SFC_OK) return rc;
+  } else {
+    pl->tile = tile_from_api(tile_api);
+  }
   pl->bm = sfc::tile_bm(pl->tile);
   pl->bn = sfc::tile_bn(pl->tile);
   pl->gm = (int)sfc::ceil_div(M, pl->bm);
   pl->gn = (int)sfc::ceil_div(N, pl->bn);
   pl->nk = (int)(K > 0 ? sfc::ceil_div(K, sfc::kBK) : 0);
-  // the fast path needs at least one K block per task
-  pl->vec = K > 0 && sfc::vector_loads_ok(A, lda, B, ldb, K, N);
   // layer copies are fp32 whatever the output type
   const bool kernel_bf16 = ob && pl->ce == 1;
-  int rc = get_occupancy(st, pl->tile, kernel_bf16, pl->vec, &pl->occ);
+  rc = get_occupancy(st, pl->tile, kernel_bf16, pl->vec, &pl->occ);
   if (rc != SFC_OK) return rc;
   const int64_t tasks = (int64_t)pl->gm * pl->gn * pl->ce;
   int64_t slots = (int64_t)st.num_cus * pl->occ;

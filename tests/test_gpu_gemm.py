@@ -50,6 +50,19 @@ def test_ragged_shapes_bf16_out(M, N, K, tile):
     ocheck.assert_gemm_close(C, Cr, R, f"bf16 {M}x{N}x{K} {tile}")
 
 
+# K depths that give the fast path 1 .. 5 blocks per task, with and without a
+# last block that runs past K (K % 64 in {8, 24, 32, 40}), split over 1-3 layers.
+@pytest.mark.parametrize("K", [8, 24, 40, 64, 72, 96, 120, 136, 160, 200, 296, 320])
+@pytest.mark.parametrize("tile", TILES)
+def test_k_depths_and_tails_fast_path(K, tile):
+    M, N = 264, 520
+    A, B = operands(M, N, K, 700 + K)
+    Cr, R = oracle(A, B, M, N, K)
+    for c in (1, 2, 3):
+        C = run_gemm(A, B, M, N, K, tile=tile, ca_layers=c)
+        ocheck.assert_gemm_close(C, Cr, R, f"K={K} {tile} c={c}")
+
+
 @pytest.mark.parametrize("tile", TILES)
 def test_vector_and_element_loads_agree_bitwise(tile):
     # lda, ldb multiples of 8 take 128-bit loads; odd ones take element loads.
