@@ -142,7 +142,24 @@ def main():
     value = g.flops / (ms_per_step * 1e-3) / 1e12
     achieved = g.flops / (kern_ms * 1e-3) / 1e12
     log(f"[bench] headline {value:.1f} TFLOP/s (wall), kernel {kern_ms:.3f} ms -> {achieved:.1f} TFLOP/s")
-    del dA, dB, C
+
+    # The vendor library on the same operands (torch.matmul -> hipBLASLt), timed
+    # the same way: a reference point, not part of the path.
+    ref = torch.empty_like(C)
+    for _ in range(args.warmup):
+        torch.matmul(dA, dB, out=ref)
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    for s0, s1 in ev:
+        s0.record(stream)
+        torch.matmul(dA, dB, out=ref)
+        s1.record(stream)
+    torch.cuda.synchronize()
+    lib_ms = sum(a.elapsed_time(b) for a, b in ev) / args.steps
+    library = {"call": "torch.matmul (hipBLASLt), bf16 in, bf16 out", "ms": round(lib_ms, 4),
+               "tflops": round(g.flops / (lib_ms * 1e-3) / 1e12, 1)}
+    log(f"[bench] library {library}")
+    del dA, dB, C, ref
     torch.cuda.empty_cache()
 
     # ---------------------------------------------- sustained MFMA throughput
@@ -244,6 +261,7 @@ def main():
                      "mfma_probe": probe,
                      "frac_of_probe_random": round(achieved / probe["random_operands"]["tflops"], 4)},
         "cpu_baseline": cpu,
+        "library_same_workload": library,
         "workloads": table,
     }
     print(json.dumps(line), flush=True)
