@@ -484,8 +484,13 @@ __device__ __forceinline__ void main_loop_ring(const RingAddr<BM, BN>& ra, int n
 #pragma unroll
     for (int j = 0; j < Tile<BM, BN>::FN; ++j) b_base[j] = bs + o.b_rd[0][j];
     const uint32_t as = ra.a_slot(0) + o.a_rd[0];
+    // same order as the reads issued by the loop's last step, so that the
+    // first MFMAs wait only for their own operands on either path into the loop
 #pragma unroll
-    for (int t = 0; t < Tile<BM, BN>::FM + Tile<BM, BN>::FN; ++t) read_item<BM, BN>(t, as, b_base, f0);
+    for (int t = 0; t < Tile<BM, BN>::FM + Tile<BM, BN>::FN; ++t) {
+      read_item<BM, BN>(t, as, b_base, f0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
   }
   for (int b = 0; b < nb; ++b) {
     const int x0 = 2 * b;
