@@ -106,6 +106,14 @@ __device__ __forceinline__ u32x4 load_chunk(const uint16_t* base, int64_t ld, in
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 constexpr int kOobOffset = 0x7FFFFFF0;   // num_records; a lane at this offset reads zeros
 
+// One 32-bit scalar load from global memory (the table written by an earlier
+// dispatch), waited for at once.
+__device__ __forceinline__ int load_scalar_i32(const int32_t* p) {
+  int v;
+  asm volatile("s_load_dword %0, %1, 0x0\n\ts_waitcnt lgkmcnt(0)" : "=s"(v) : "s"(p) : "memory");
+  return v;
+}
+
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
 }
@@ -647,31 +655,37 @@ __global__ __launch_bounds__(kThreads, 1) void sfc_gemm_kernel(GemmParams p) {
 
   const int P = gridDim.x;
   const int rank = xcd_rank(blockIdx.x, P);
-  const int64_t NT = p.tasks;
-  int64_t t_begin, t_end, t_step;
+  // task counts are below 2^31 (the library checks it), so 32-bit indices do
+  const int NT = (int)p.tasks;
+  int t_begin, t_end, t_step;
   if (p.sched == 1) {                  // block partition
-    t_begin = NT * rank / P;
-    t_end = NT * (rank + 1) / P;
+    t_begin = (int)((int64_t)NT * rank / P);
+    t_end = (int)((int64_t)NT * (rank + 1) / P);
     t_step = 1;
   } else {                             // interleaved
     t_begin = rank;
     t_end = NT;
     t_step = P;
   }
-  const int64_t cells = (int64_t)p.gm * p.gn;
+  const int cells = p.gm * p.gn;
   // 4-wide stores need 4-element aligned rows (and layer copies).
   const int esize = OUT_BF16 ? 2 : 4;
   const bool vec_store = ((uintptr_t)p.out % (4 * esize)) == 0 && (p.ldo % 4) == 0 &&
                          (p.out_layer_stride % 4) == 0;
 
-  for (int64_t t = t_begin; t < t_end; t += t_step) {
-    const int layer = (int)(t / cells);
-    const int s = (int)(t - (int64_t)layer * cells);
-    const int cell = p.table[s];
+  for (int t = t_begin; t < t_end; t += t_step) {
+    // Per-lane values are recomputed for every task rather than kept live
+    // across the whole kernel (that costs registers the main loop needs).
+    int lane_t;
+    asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(lane_t));
+    const int layer = t / cells;
+    const int s = t - layer * cells;
+    // scalar load: a vector load here would wait for the previous task's stores
+    const int cell = load_scalar_i32(p.table + s);
     const int im = cell / p.gn, in = cell - im * p.gn;
     const int64_t m0 = (int64_t)im * BM, n0 = (int64_t)in * BN;
-    const int kt0 = (int)((int64_t)layer * p.nk / p.layers);
-    const int kt1 = (int)((int64_t)(layer + 1) * p.nk / p.layers);
+    const int kt0 = (int)((unsigned)layer * (unsigned)p.nk / (unsigned)p.layers);
+    const int kt1 = (int)((unsigned)(layer + 1) * (unsigned)p.nk / (unsigned)p.layers);
 
     f32x16 acc[T::FM][T::FN];
 #pragma unroll
@@ -686,14 +700,14 @@ __global__ __launch_bounds__(kThreads, 1) void sfc_gemm_kernel(GemmParams p) {
         // a last block that runs past K is loaded with per-lane masks
         const int64_t kin_last = p.K - (int64_t)(kt1 - 1) * kBK;
         RingLanes<BM, BN> L;
-        ring_lanes<BM, BN>(p, m0, n0, wave, lane, L);
+        ring_lanes<BM, BN>(p, m0, n0, wave, lane_t, L);
         RingAddr<BM, BN> ra;
         ra.a0 = reinterpret_cast<uint64_t>(p.A + m0 * p.lda + (int64_t)kt0 * kBK) - kBias;
         ra.b0 = reinterpret_cast<uint64_t>(p.B + (int64_t)kt0 * kBK * p.ldb + n0) - kBias;
         ra.b_step = (uint64_t)kSK * (uint64_t)p.ldb * 2;
         ra.lds0 = lds_addr(smem);
         ra.wave = wave;
-        main_loop_ring<BM, BN>(ra, kt1 - kt0, kin_last, ro, L, lane, acc);
+        main_loop_ring<BM, BN>(ra, kt1 - kt0, kin_last, ro, L, lane_t, acc);
       } else {
         main_loop_staged<BM, BN>(p, smem, m0, n0, kt0, kt1, tid, acc);
       }
@@ -703,7 +717,7 @@ __global__ __launch_bounds__(kThreads, 1) void sfc_gemm_kernel(GemmParams p) {
     // column 8*(e/4) + 4*(lane/32) + e%4 of that 32x32 fragment.
     const int64_t lstride = p.out_layer_stride * layer;
     const bool interior = m0 + BM <= p.M && n0 + BN <= p.N;
-    store_tile<BM, BN, OUT_BF16>(p, acc, m0, n0, lstride, wm, wn, lane, interior && vec_store);
+    store_tile<BM, BN, OUT_BF16>(p, acc, m0, n0, lstride, wm, wn, lane_t, interior && vec_store);
   }
 }
 
