@@ -10,7 +10,7 @@
 //
 // Mapping to the chip:
 //   * one workgroup = 4 waves (2 x 2), each wave owns a (BM/2) x (BN/2)
-//     sub-block held as 32x32 fp32 MFMA accumulators;
+//     sub-block held as 16x16 fp32 MFMA accumulators;
 //   * the grid is persistent: P workgroups, P = CUs x occupancy, each looping
 //     over tasks.  Hardware deals workgroup b to chiplet (XCD) b % 8; ranks are
 //     renumbered so that each XCD's workgroups hold consecutive ranks, and with
@@ -29,7 +29,9 @@
 //     (ds_read_b64_tr_b16); 16-byte chunks are XOR-swizzled so that the
 //     fragment reads and the staging writes are free of bank conflicts on the
 //     64-bank LDS;
-//   * bf16 MFMA 32x32x16 with fp32 accumulation (Section III.A's BRGEMM role).
+//   * bf16 MFMA 16x16x32 with fp32 accumulation (Section III.A's BRGEMM role).
+//     With random operands it holds a higher clock than 32x32x16 for the same
+//     work per clock.
 #include <type_traits>
 #include <utility>
 
@@ -40,10 +42,12 @@ namespace sfc {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef short i16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+typedef __attribute__((address_space(3))) const bf16x8 lds_bf16x8;
 
 // ---- chiplet-aware rank ------------------------------------------------------
 // Workgroup b runs on XCD b % 8.  Ranks give each XCD a contiguous range.
@@ -55,21 +59,20 @@ __device__ __forceinline__ int xcd_rank(int b, int P) {
 }
 
 // ---- LDS layouts ---------------------------------------------------------------
-// A block: [BM rows][KW k] bf16, KW/8 chunks of 16 B per row, chunk c of row r
-// stored at c ^ swizzle(r).  KW = 64 (general path): c ^ ((r >> 1) & 7); KW =
-// 32 (ring slots): c ^ ((r >> 2) & 3).  Either way the 16 rows that one quarter
+// A block: [BM rows][64 k] bf16, 8 chunks of 16 B per row; chunk c of row r is
+// stored at chunk c ^ ((r >> 1) & 7).  The 16 consecutive rows that one quarter
 // of a wave reads at one logical chunk land on 16 distinct 16-byte bank groups.
-template <int KW>
 __device__ __forceinline__ int a_off(int row, int chunk) {
-  if constexpr (KW == 64) return row * 64 + ((chunk ^ ((row >> 1) & 7)) << 3);
-  else return row * 32 + ((chunk ^ ((row >> 2) & 3)) << 3);
+  return row * kBK + ((chunk ^ ((row >> 1) & 7)) << 3);
 }
-// B block: [K k][BN n] bf16 (K = 64 or 32); chunk c (8 columns) of row k is stored at chunk
-// c ^ ((k & 3) << 2).  The transposing read touches 4 rows x 4 chunks per
-// 32 lanes, which this spreads over all 16 bank groups.
+// B block: [K k][BN n] bf16 (K = 64 or 32); chunk c (8 columns) of row k is
+// stored at chunk c ^ b_swz(k).  One pass of the transposing read (32 lanes)
+// touches rows k0..k0+3 and k0+8..k0+11 at 2 chunks; the swizzle puts those 16
+// pieces on 16 distinct 16-byte bank groups.
+__device__ __forceinline__ int b_swz(int k) { return ((k & 3) << 2) | (((k >> 3) & 1) << 1); }
 template <int BN>
 __device__ __forceinline__ int b_off(int k, int n) {
-  return k * BN + ((((n >> 3) ^ ((k & 3) << 2))) << 3) + (n & 7);
+  return k * BN + ((((n >> 3) ^ b_swz(k))) << 3) + (n & 7);
 }
 
 // ---- global -> register staging -------------------------------------------------
@@ -98,13 +101,13 @@ __device__ __forceinline__ u32x4 load_chunk(const uint16_t* base, int64_t ld, in
 // ---- direct global -> LDS loads (fast path) ----------------------------------------
 // buffer_load_dwordx4 ... offset:O lds: every lane fetches 16 bytes at (descriptor
 // base + its voffset + O) and the wave writes them to LDS at M0 + O + 16*lane.  A
-// lane whose voffset lies at or beyond the descriptor's num_records fetches
+// lane whose voffset + O lies at or beyond the descriptor's num_records fetches
 // zeros.  The instruction is issued from inline assembly so that the compiler
 // does not serialise later LDS reads behind it; the kernel orders it explicitly
 // with s_waitcnt vmcnt and workgroup barriers.  Raw buffer descriptor: 48-bit
 // base, stride 0, num_records, word 3 = 0x00020000 on gfx9 parts.
 typedef int i32x4 __attribute__((ext_vector_type(4)));
-constexpr int kOobOffset = 0x7FFFFFF0;   // num_records; a lane at this offset reads zeros
+constexpr int kOobOffset = 0x7FFFFFF0;   // largest num_records; a lane at this offset reads zeros
 
 // One 32-bit scalar load from global memory (the table written by an earlier
 // dispatch), waited for at once.
@@ -125,18 +128,21 @@ __device__ __forceinline__ void wait_vmem_at_most() {
 }
 __device__ __forceinline__ void wait_lds_all() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 
-// ---- one K block of MFMA work ----------------------------------------------------------
+// ---- MFMA 16x16x32 fragments -------------------------------------------------------------
+// The MFMA takes the B fragment as its first operand, so it computes the
+// transposed 16x16 block: lane l ends with row l%16 of the fragment and its 4
+// consecutive columns 4*(l/16) .. +3.
 template <int BM, int BN>
 struct Tile {
   static constexpr int WTM = BM / 2, WTN = BN / 2;   // wave sub-block (2 x 2 waves)
-  static constexpr int FM = WTM / 32, FN = WTN / 32; // 32x32 fragments per wave
+  static constexpr int FM = WTM / 16, FN = WTN / 16; // 16x16 fragments per wave
   static constexpr int A_ELEMS = BM * kBK, B_ELEMS = kBK * BN;
   static constexpr int A_CH = BM * kBK / 8 / kThreads;   // 16-byte chunks per thread
   static constexpr int B_CH = kBK * BN / 8 / kThreads;
 };
 
 template <int BM, int BN>
-using Acc = f32x16[Tile<BM, BN>::FM][Tile<BM, BN>::FN];
+using Acc = f32x4[Tile<BM, BN>::FM][Tile<BM, BN>::FN];
 
 template <int BM, int BN>
 struct Frags {
@@ -144,72 +150,74 @@ struct Frags {
   bf16x8 b[Tile<BM, BN>::FN];
 };
 
-// A operand fragment i of k sub-step ks (16 deep): lane holds row lane%32,
-// k = 8*(lane/32) .. +8.
-template <int BM, int BN, int KW>
-__device__ __forceinline__ void read_a(const uint16_t* As, int wm, int lane, int ks, int i,
-                                       Frags<BM, BN>& f) {
-  using T = Tile<BM, BN>;
-  const int row = wm * T::WTM + i * 32 + (lane & 31);
-  const int c = ks * 2 + (lane >> 5);
-  f.a[i] = *reinterpret_cast<const bf16x8*>(As + a_off<KW>(row, c));
+// Per-lane LDS element offsets of the fragment reads of one 32-deep step:
+// A fragment i of step ks (0 or 1 within a 64-deep block) is 16 rows x 32 k,
+// lane l holding row l%16, k = 8*(l/16) .. +8; the swizzle does not depend on
+// i, so fragment i sits i*16*64 elements further.  B fragment j is 32 k x 16
+// columns, lane l holding column l%16, k = 8*(l/16) .. +8, assembled from two
+// transposing reads of 4 rows each (the second 4 rows further).
+__device__ __forceinline__ int a_frag_off(int wm_rows, int lane, int ks) {
+  const int row = wm_rows + (lane & 15);
+  return a_off(row, ks * 4 + (lane >> 4));
 }
-// B operand fragment j: lane holds column lane%32, k = 8*(lane/32) .. +8.  Lane
-// (g = lane/16, jj = lane%16) points at row k, columns n..n+3; the transposing
-// read returns column n0 + jj of rows k0..k0+3 to lane jj.
-template <int BM, int BN>
-__device__ __forceinline__ void read_b(const uint16_t* Bs, int wn, int lane, int ks, int j,
-                                       Frags<BM, BN>& f) {
-  using T = Tile<BM, BN>;
+template <int BN>
+__device__ __forceinline__ int b_frag_off(int wn_cols, int lane, int kbase, int j) {
+  // Lane (g = l/16, jj = l%16) points at row 8g + jj/4, columns n .. n+3 with
+  // n = 16j + 4*(jj%4); the transposing read returns column jj of the 4 rows
+  // to lane jj of each group of 16.
   const int g = lane >> 4, jj = lane & 15;
-  const int n = wn * T::WTN + j * 32 + ((g & 1) << 4) + ((jj & 3) << 2);
-  const int k = ks * 16 + ((g >> 1) << 3) + (jj >> 2);
-  const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(Bs + b_off<BN>(k, n)));
-  const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(Bs + b_off<BN>(k + 4, n)));
-  const i16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-  f.b[j] = __builtin_bit_cast(bf16x8, v);
-}
-// All operand fragments of k sub-step ks for this lane.
-template <int BM, int BN, int KW>
-__device__ __forceinline__ void load_frags(const uint16_t* As, const uint16_t* Bs, int wm, int wn,
-                                           int lane, int ks, Frags<BM, BN>& f) {
-  using T = Tile<BM, BN>;
-#pragma unroll
-  for (int i = 0; i < T::FM; ++i) read_a<BM, BN, KW>(As, wm, lane, ks, i, f);
-#pragma unroll
-  for (int j = 0; j < T::FN; ++j) read_b<BM, BN>(Bs, wn, lane, ks, j, f);
+  const int k = kbase + 8 * g + (jj >> 2);
+  const int n = wn_cols + j * 16 + ((jj & 3) << 2);
+  return b_off<BN>(k, n);
 }
 
-// acc += one 16-deep step.
+__device__ __forceinline__ bf16x8 read_b_pair(const uint16_t* p, int half_stride) {
+  const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p);
+  const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p + half_stride));
+  const i16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  return __builtin_bit_cast(bf16x8, v);
+}
+
+// All operand fragments of one 32-deep step from an A block [BM][64] (step
+// ks) and a B buffer [..][BN] (rows kbase .. kbase+31).
 template <int BM, int BN>
-__device__ __forceinline__ void mma_step(const Frags<BM, BN>& cur,
-                                         f32x16 (&acc)[Tile<BM, BN>::FM][Tile<BM, BN>::FN]) {
+__device__ __forceinline__ void load_frags(const uint16_t* As, const uint16_t* Bs, int wm, int wn,
+                                           int lane, int ks, int kbase, Frags<BM, BN>& f) {
+  using T = Tile<BM, BN>;
+  const int ao = a_frag_off(wm * T::WTM, lane, ks);
+#pragma unroll
+  for (int i = 0; i < T::FM; ++i) f.a[i] = *reinterpret_cast<const bf16x8*>(As + ao + i * 16 * kBK);
+#pragma unroll
+  for (int j = 0; j < T::FN; ++j) f.b[j] = read_b_pair(Bs + b_frag_off<BN>(wn * T::WTN, lane, kbase, j), 4 * BN);
+}
+
+// acc += one 32-deep step.
+template <int BM, int BN>
+__device__ __forceinline__ void mma_step(const Frags<BM, BN>& cur, Acc<BM, BN>& acc) {
   using T = Tile<BM, BN>;
 #pragma unroll
   for (int i = 0; i < T::FM; ++i)
 #pragma unroll
     for (int j = 0; j < T::FN; ++j)
-      // B fragment as the first operand: the accumulator holds the transposed
-      // 32x32 block, so each lane ends with runs of 4 consecutive columns.
-      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cur.b[j], cur.a[i], acc[i][j], 0, 0, 0);
+      acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(cur.b[j], cur.a[i], acc[i][j], 0, 0, 0);
 }
 
 // ---- fast path: rings of LDS slots ---------------------------------------------------------
-// A is staged per 64-deep block, in three slots of [BM][64] (a_off<64>): a row of
-// a block is one full 128-byte line of A.  B is staged per 32-deep stage, in
-// four slots of [32][BN] (b_off).  Loads are buffer loads of 1 KiB (16 B per
-// lane) written straight into LDS.  Wave w loads A segments w*APB .. +APB-1
-// (8 rows each) of a block and B segments w*BPW .. +BPW-1 of a stage; a wave's
-// segments are consecutive KiB, so up to four share one M0 value and differ
-// only in the instruction offset, which the hardware adds to both the LDS
-// address and the memory address.  The per-lane voffset is biased by kBias -
-// offset and the descriptor base lowered by kBias to cancel the memory side.
+// A is staged per 64-deep block, in three slots of [BM][64]: a row of a block is
+// one full 128-byte line of A.  B is staged per 32-deep stage, in four slots of
+// [32][BN].  A 32-deep stage is one MFMA step.  Loads are buffer loads of 1 KiB
+// (16 B per lane) written straight into LDS.  Wave w loads A segments w*APB ..
+// +APB-1 (8 rows each) of a block and B segments w*BPW .. +BPW-1 of a stage; a
+// wave's segments are consecutive KiB, so up to four share one M0 value and
+// differ only in the instruction offset, which the hardware adds to both the
+// LDS address and the memory address.  The per-lane voffset is biased by kBias
+// - offset and the descriptor base lowered by kBias to cancel the memory side.
 //
 // Every instruction of the loop counts: with one wave per SIMD a wave issues
-// at most one instruction per four clocks, and an MFMA 32x32x16 occupies the
-// matrix core for 32, so the loop keeps its other work (LDS reads, loads,
-// address arithmetic) to a few instructions per MFMA, spread evenly.
-constexpr int kSK = 32;        // K depth of one B stage
+// at most one instruction per four clocks, so the loop keeps its other work
+// (LDS reads, loads, address arithmetic) to a few instructions per MFMA,
+// spread evenly.
+constexpr int kSK = 32;        // K depth of one B stage (one MFMA step)
 constexpr int kASlots = 3;     // A block slots
 constexpr int kBSlots = 4;     // B stage slots
 constexpr int kBias = 4096;    // bytes; keeps every biased voffset positive
@@ -236,10 +244,11 @@ __device__ __forceinline__ void dma16_pair(i32x4 rsrc, uint32_t m0_value, int v0
                :: "s"(m0_value), "v"(v0), "v"(v1), "s"(rsrc), "n"(OFF), "n"(OFF + 1024) : "memory");
 }
 
-__device__ __forceinline__ i32x4 make_rsrc_addr(uint64_t a) {
-  i32x4 r = {(int)(uint32_t)a, (int)((uint32_t)(a >> 32) & 0xFFFFu), kOobOffset, 0x00020000};
+__device__ __forceinline__ i32x4 make_rsrc_addr(uint64_t a, uint32_t num_records) {
+  i32x4 r = {(int)(uint32_t)a, (int)((uint32_t)(a >> 32) & 0xFFFFu), (int)num_records, 0x00020000};
   r[0] = __builtin_amdgcn_readfirstlane(r[0]);
   r[1] = __builtin_amdgcn_readfirstlane(r[1]);
+  r[2] = __builtin_amdgcn_readfirstlane(r[2]);
   return r;
 }
 
@@ -250,14 +259,10 @@ struct RingLanes {
   int b_voff[Ring<BM, BN>::BPW];
 };
 
-// K index (within a block or stage) at which load j of this lane starts.
+// K index (within a block) at which A load j of this lane starts.
 __device__ __forceinline__ int a_load_k(int wave, int apb, int j, int lane) {
   const int row = (wave * apb + j) * 8 + (lane >> 3);
   return ((lane & 7) ^ ((row >> 1) & 7)) * 8;
-}
-template <int BN>
-__device__ __forceinline__ int b_load_k(int wave, int bpw, int j, int lane) {
-  return ((wave * bpw + j) * 512 + lane * 8) / BN;
 }
 
 template <int BM, int BN>
@@ -274,40 +279,38 @@ __device__ __forceinline__ void ring_lanes(const GemmParams& p, int64_t m0, int6
   for (int j = 0; j < R::BPW; ++j) {
     const int e = (wave * R::BPW + j) * 512 + lane * 8;   // element index in the [32][BN] stage
     const int k = e / BN;
-    const int c = ((e % BN) >> 3) ^ ((k & 3) << 2);
+    const int c = ((e % BN) >> 3) ^ b_swz(k);
     L.b_voff[j] = (n0 + c * 8 < p.N) ? (int)((k * p.ldb + c * 8) * 2) + kBias - j * 1024 : kOobOffset;
   }
 }
 
+// Turn the A lanes whose load starts at a K index >= kin (within the block)
+// into out-of-range lanes, for the loads of a block that runs past K.
+template <int BM, int BN>
+__device__ __forceinline__ void mask_a_lanes(RingLanes<BM, BN>& L, int wave, int lane, int64_t kin) {
+  using R = Ring<BM, BN>;
+#pragma unroll
+  for (int j = 0; j < R::APB; ++j)
+    if (a_load_k(wave, R::APB, j, lane) >= kin) L.a_voff[j] = kOobOffset;
+}
+
 // Per-lane LDS byte offsets of the fragment reads within a slot: A fragment i
-// of 16-deep sub-step ka (0..3 within a block) at a_rd[ka] + i*4096 (the
-// swizzle does not depend on i); the two halves of B fragment j of sub-step ks
-// (0..1 within a stage) at b_rd[ks][j] and b_rd[ks][j] + 8*BN.
+// of step ks at a_rd[ks] + i*2048; the two halves of B fragment j at b_rd[j]
+// and b_rd[j] + 8*BN.
 template <int BM, int BN>
 struct ReadOffsets {
-  uint32_t a_rd[4];
-  uint32_t b_rd[2][Tile<BM, BN>::FN];
+  uint32_t a_rd[2];
+  uint32_t b_rd[Tile<BM, BN>::FN];
 };
 
 template <int BM, int BN>
 __device__ __forceinline__ void read_offsets(int wm, int wn, int lane, ReadOffsets<BM, BN>& o) {
   using T = Tile<BM, BN>;
-  const int row = wm * T::WTM + (lane & 31);
 #pragma unroll
-  for (int ka = 0; ka < 4; ++ka) o.a_rd[ka] = (uint32_t)(a_off<64>(row, ka * 2 + (lane >> 5)) * 2);
-  const int g = lane >> 4, jj = lane & 15;
+  for (int ks = 0; ks < 2; ++ks) o.a_rd[ks] = (uint32_t)(a_frag_off(wm * T::WTM, lane, ks) * 2);
 #pragma unroll
-  for (int ks = 0; ks < 2; ++ks) {
-    const int k = ks * 16 + ((g >> 1) << 3) + (jj >> 2);
-#pragma unroll
-    for (int j = 0; j < T::FN; ++j) {
-      const int n = wn * T::WTN + j * 32 + ((g & 1) << 4) + ((jj & 3) << 2);
-      o.b_rd[ks][j] = (uint32_t)(b_off<BN>(k, n) * 2);
-    }
-  }
+  for (int j = 0; j < T::FN; ++j) o.b_rd[j] = (uint32_t)(b_frag_off<BN>(wn * T::WTN, lane, 0, j) * 2);
 }
-
-typedef __attribute__((address_space(3))) const bf16x8 lds_bf16x8;
 
 // Read item t of a step, in the order the next step's MFMAs consume them:
 // A0, B0, B1, .., B(FN-1), A1, .., A(FM-1).
@@ -316,7 +319,7 @@ __device__ __forceinline__ void read_item(int t, uint32_t a_base, const uint32_t
   using T = Tile<BM, BN>;
   if (t == 0 || t > T::FN) {
     const int i = t == 0 ? 0 : t - T::FN;
-    f.a[i] = *(lds_bf16x8*)(uintptr_t)(a_base + (uint32_t)(i * 4096));
+    f.a[i] = *(lds_bf16x8*)(uintptr_t)(a_base + (uint32_t)(i * 16 * kBK * 2));
   } else {
     const int j = t - 1;
     const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(uintptr_t)b_base[j]);
@@ -351,135 +354,158 @@ __device__ __forceinline__ void dma_all(const SlotDma& d, const RingLanes<BM, BN
   }(std::make_integer_sequence<int, (OP == 1 ? R::APB : R::BPW) / 2>{});
 }
 
-// Turn the lanes whose load starts at a K index >= kin (within the block or
-// stage) into out-of-range lanes, for the loads of a block that runs past K.
-// Applied once more with a smaller kin it only masks further.
-template <int BM, int BN, bool A, bool B>
-__device__ __forceinline__ void mask_lanes(RingLanes<BM, BN>& L, int wave, int lane, int64_t kin) {
-  using R = Ring<BM, BN>;
-  if constexpr (A) {
-#pragma unroll
-    for (int j = 0; j < R::APB; ++j)
-      if (a_load_k(wave, R::APB, j, lane) >= kin) L.a_voff[j] = kOobOffset;
-  }
-  if constexpr (B) {
-#pragma unroll
-    for (int j = 0; j < R::BPW; ++j)
-      if (b_load_k<BN>(wave, R::BPW, j, lane) >= kin) L.b_voff[j] = kOobOffset;
+// One group of a step: MFMA g, then the reads and the load pair that fall on g.
+template <int BM, int BN, int OP, int g, int... t>
+__device__ __forceinline__ void group_reads(uint32_t a_base, const uint32_t* b_base, Frags<BM, BN>& nxt,
+                                            std::integer_sequence<int, t...>) {
+  using T = Tile<BM, BN>;
+  constexpr int G = T::FM * T::FN, NI = T::FM + T::FN;
+  ((void)((t * G) / NI == g ? (read_item<BM, BN>(t, a_base, b_base, nxt), 0) : 0), ...);
+}
+
+template <int BM, int BN, int OP>
+struct StepLoads {
+  static constexpr int NP0 = OP == 1 ? Ring<BM, BN>::APB / 2 : Ring<BM, BN>::BPW / 2;   // pairs from d0
+  static constexpr int NP1 = OP == 1 ? 0 : Ring<BM, BN>::BPW / 2;                      // pairs from d1
+  static constexpr int NP = NP0 + NP1;
+};
+
+template <int BM, int BN, int OP, int g, int q>
+__device__ __forceinline__ void group_load(const SlotDma& d0, const SlotDma& d1, const RingLanes<BM, BN>& L) {
+  using T = Tile<BM, BN>;
+  using S = StepLoads<BM, BN, OP>;
+  constexpr int G = T::FM * T::FN;
+  if constexpr (((2 * q + 1) * G) / (2 * S::NP) == g) {
+    if constexpr (q < S::NP0) dma_pair<BM, BN, OP, q>(d0, L);
+    else dma_pair<BM, BN, OP, q - S::NP0>(d1, L);
   }
 }
 
-// One 16-deep step with a fixed instruction order: group g issues MFMA g of
-// `cur` (i-major), then the fragment reads of `nxt` that fall on g, then the
-// load pair that falls on g.  Loads: pairs [Q0, Q1) of an A block (OP 1) or
-// of a B stage (OP 2), spread evenly over the groups so that neither the LDS
-// nor the texture path receives a burst.
-template <int BM, int BN, int OP, int Q0, int Q1>
-__device__ __forceinline__ void ring_step(Acc<BM, BN>& acc, const Frags<BM, BN>& cur, Frags<BM, BN>& nxt,
-                                          uint32_t a_base, uint32_t b_slot, int ks,
-                                          const ReadOffsets<BM, BN>& o, bool dma_on, const SlotDma& d,
-                                          const RingLanes<BM, BN>& L) {
+template <int BM, int BN, int OP, int g, int... q>
+__device__ __forceinline__ void group_loads(const SlotDma& d0, const SlotDma& d1, const RingLanes<BM, BN>& L,
+                                            std::integer_sequence<int, q...>) {
+  (group_load<BM, BN, OP, g, q>(d0, d1, L), ...);
+}
+
+template <int BM, int BN, int OP, int g>
+__device__ __forceinline__ void ring_group(Acc<BM, BN>& acc, const Frags<BM, BN>& cur, Frags<BM, BN>& nxt,
+                                           uint32_t a_base, const uint32_t* b_base, const SlotDma& d0,
+                                           const SlotDma& d1, const RingLanes<BM, BN>& L) {
   using T = Tile<BM, BN>;
-  constexpr int G = T::FM * T::FN;
-  constexpr int NI = T::FM + T::FN;
-  constexpr int NP = Q1 - Q0;
+  constexpr int i = g / T::FN, j = g % T::FN;
+  acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(cur.b[j], cur.a[i], acc[i][j], 0, 0, 0);
+  group_reads<BM, BN, OP, g>(a_base, b_base, nxt, std::make_integer_sequence<int, T::FM + T::FN>{});
+  group_loads<BM, BN, OP, g>(d0, d1, L, std::make_integer_sequence<int, StepLoads<BM, BN, OP>::NP>{});
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+template <int BM, int BN, int OP, int... g>
+__device__ __forceinline__ void ring_groups(Acc<BM, BN>& acc, const Frags<BM, BN>& cur, Frags<BM, BN>& nxt,
+                                            uint32_t a_base, const uint32_t* b_base, const SlotDma& d0,
+                                            const SlotDma& d1, const RingLanes<BM, BN>& L,
+                                            std::integer_sequence<int, g...>) {
+  (ring_group<BM, BN, OP, g>(acc, cur, nxt, a_base, b_base, d0, d1, L), ...);
+}
+
+// One 32-deep step with a fixed instruction order: group g issues MFMA g of
+// `cur` (i-major), then the fragment reads of `nxt` that fall on g, then the
+// load pair that falls on g.  Loads: the pairs of an A block d0 (OP 1), or the
+// pairs of two B stages d0 and d1 (OP 2), spread evenly over the groups so
+// that neither the LDS nor the texture path receives a burst.  The groups are
+// generated as straight-line code (a loop this long is not always unrolled,
+// and the accumulators must stay in registers).
+template <int BM, int BN, int OP>
+__device__ __forceinline__ void ring_step(Acc<BM, BN>& acc, const Frags<BM, BN>& cur, Frags<BM, BN>& nxt,
+                                          uint32_t a_base, uint32_t b_slot, const ReadOffsets<BM, BN>& o,
+                                          const SlotDma& d0, const SlotDma& d1, const RingLanes<BM, BN>& L) {
+  using T = Tile<BM, BN>;
   uint32_t b_base[T::FN];
 #pragma unroll
-  for (int j = 0; j < T::FN; ++j) b_base[j] = b_slot + o.b_rd[ks][j];
-#pragma unroll
-  for (int g = 0; g < G; ++g) {
-    const int i = g / T::FN, j = g % T::FN;
-    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cur.b[j], cur.a[i], acc[i][j], 0, 0, 0);
-#pragma unroll
-    for (int t = 0; t < NI; ++t)
-      if ((t * G) / NI == g) read_item<BM, BN>(t, a_base, b_base, nxt);
-    if constexpr (NP > 0) {
-      if (dma_on) {
-        [&]<int... q>(std::integer_sequence<int, q...>) {
-          ((void)(((2 * q + 1) * G) / (2 * NP) == g ? (dma_pair<BM, BN, OP, Q0 + q>(d, L), 0) : 0), ...);
-        }(std::make_integer_sequence<int, NP>{});
-      }
-    }
-    __builtin_amdgcn_sched_barrier(0);
-  }
+  for (int j = 0; j < T::FN; ++j) b_base[j] = b_slot + o.b_rd[j];
+  ring_groups<BM, BN, OP>(acc, cur, nxt, a_base, b_base, d0, d1, L,
+                          std::make_integer_sequence<int, T::FM * T::FN>{});
 }
 
-// Where the blocks and stages of one task come from and go to.
-template <int BM, int BN>
+// Where the blocks and stages of one task come from and go to.  Everything
+// here is wave-uniform (scalar registers).
 struct RingAddr {
   uint64_t a0, b0;           // byte address of the first block's A origin and B origin, minus kBias
   uint64_t b_step;           // bytes between consecutive B stages (32 rows of B)
+  int b_rows;                // rows of B from the first stage's origin to row K
+  int ldb2;                  // bytes per row of B
   uint32_t lds0;             // LDS byte address of the ring
   int wave;
-  // A block kb: descriptor and this wave's M0 in A slot kb mod 3
-  __device__ __forceinline__ SlotDma a_blk(int kb) const {
-    using R = Ring<BM, BN>;
-    SlotDma d;
-    d.rsrc = make_rsrc_addr(a0 + (uint64_t)kb * (kBK * 2));
-    d.m0 = lds0 + (uint32_t)((kb % kASlots) * R::A_BYTES + wave * R::APB * 1024);
-    return d;
-  }
-  // B stage x: descriptor and this wave's M0 in B slot x mod 4
-  __device__ __forceinline__ SlotDma b_stg(int x) const {
-    using R = Ring<BM, BN>;
-    SlotDma d;
-    d.rsrc = make_rsrc_addr(b0 + (uint64_t)x * b_step);
-    d.m0 = lds0 + (uint32_t)(R::B_OFF + (x & (kBSlots - 1)) * R::B_BYTES + wave * R::BPW * 1024);
-    return d;
-  }
-  // LDS byte addresses of the slots, materialised as scalars so that the
-  // fragment reads add them once per base address and fold the rest into
-  // their immediate offsets
-  __device__ __forceinline__ uint32_t a_slot(int kb) const {
-    return (uint32_t)__builtin_amdgcn_readfirstlane((int)(lds0 + (uint32_t)((kb % kASlots) * Ring<BM, BN>::A_BYTES)));
-  }
-  __device__ __forceinline__ uint32_t b_slot(int x) const {
-    using R = Ring<BM, BN>;
-    return (uint32_t)__builtin_amdgcn_readfirstlane((int)(lds0 + (uint32_t)(R::B_OFF + (x & (kBSlots - 1)) * R::B_BYTES)));
-  }
 };
 
+// num_records of B stage x: rows at or past K fall outside and read zeros (a
+// stage wholly past K reads nothing from memory)
+__device__ __forceinline__ uint32_t b_stage_limit(const RingAddr& ra, int x) {
+  const int rows = min(max(ra.b_rows - x * kSK, 0), kSK);
+  return rows == kSK ? (uint32_t)kOobOffset : (uint32_t)(rows * ra.ldb2 + kBias);
+}
+
 // The K loop of one task over nb 64-deep blocks.  Block b = A block b and B
-// stages x0 = 2b, x0+1; its 16-deep steps are A (x0/ks0), B (x0/ks1), C
-// (x0+1/ks0), D (x0+1/ks1).  Each step runs the MFMAs of one sub-step while it
-// reads the operands of the next:
-//   step A: reads A b/1, B x0/1;    loads: B stage x0+3
-//   step B: reads A b/2, B x0+1/0;  loads: first half of A block b+2
-//   step C: reads A b/3, B x0+1/1;  loads: second half of A block b+2
-//   wait until A block b+1 and B stages <= x0+3 have landed (A block b+2 may
-//   still be in flight), barrier b
-//   step D: reads A b+1/0, B x0+2/0; loads: B stage x0+4
+// stages x0 = 2b, x0+1, one 32-deep MFMA step each.  Each step runs the MFMAs
+// of one stage while it reads the operands of the next:
+//   step 1 (MFMAs of x0, reads A b/1 and B x0+1):  loads: A block b+2
+//   wait until A block b+1 and B stages x0+2, x0+3 have landed (A block b+2
+//   may still be in flight), barrier b
+//   step 2 (MFMAs of x0+1, reads A b+1/0 and B x0+2): loads: B stages x0+4, x0+5
 // A block kb lives in A slot kb mod 3, B stage x in B slot x mod 4.  Every load
 // goes into a slot whose last reads were issued before the barrier that
 // precedes the load; the shortest lead from a load to the barrier that
-// publishes it is two steps.
+// publishes it is one step.  The per-block scalar work (descriptors, slot
+// addresses) is carried from block to block so that little of it sits between
+// MFMAs.  The last blocks still issue their loads, for blocks and stages past
+// K, with empty ranges (no memory is read, zeros land in slots that are not
+// read again), so that the loop has no branches around loads or waits.
 //
-// When the last block runs past K (kin_last < 64), its loads are the last ones
-// issued, in the order A block nb-1, B stage 2nb-2, B stage 2nb-1: the lanes
-// are masked at kin_last right before the first of them, and B once more at
-// kin_last - 32 before the last.
+// When the last block runs past K (kin_last < 64): B rows at or past K fall
+// outside the B descriptors' ranges and read zeros; A block nb-1 is loaded with
+// its lanes past K masked (the mask goes on right before those loads, which are
+// the last A loads of the task).
 template <int BM, int BN>
-__device__ __forceinline__ void main_loop_ring(const RingAddr<BM, BN>& ra, int nb, int64_t kin_last,
+__device__ __forceinline__ void main_loop_ring(const RingAddr& ra, int nb, int64_t kin_last,
                                                const ReadOffsets<BM, BN>& o, RingLanes<BM, BN>& L, int lane,
                                                Acc<BM, BN>& acc) {
   using R = Ring<BM, BN>;
-  constexpr int AH = R::APB / 4;      // load pairs per half A block
-  constexpr int BQ = R::BPW / 2;      // load pairs per B stage
+  using T = Tile<BM, BN>;
   const int wave = ra.wave;
-  const int nst = 2 * nb;
   const bool masked = kin_last < kBK;
+  const uint32_t a_m0w = (uint32_t)(wave * R::APB * 1024);          // this wave's first A segment
+  const uint32_t b_m0w = (uint32_t)(R::B_OFF + wave * R::BPW * 1024);
+  auto a_dma = [&](uint64_t addr, int slot, uint32_t lim) {
+    SlotDma d;
+    d.rsrc = make_rsrc_addr(addr, lim);
+    d.m0 = ra.lds0 + a_m0w + (uint32_t)(slot * R::A_BYTES);
+    return d;
+  };
+  auto b_dma = [&](uint64_t addr, int x) {
+    SlotDma d;
+    d.rsrc = make_rsrc_addr(addr, b_stage_limit(ra, x));
+    d.m0 = ra.lds0 + b_m0w + (uint32_t)((x & (kBSlots - 1)) * R::B_BYTES);
+    return d;
+  };
+  auto a_slot = [&](int slot) {
+    return (uint32_t)__builtin_amdgcn_readfirstlane((int)(ra.lds0 + (uint32_t)(slot * R::A_BYTES)));
+  };
+  auto b_slot = [&](int x) {
+    return (uint32_t)__builtin_amdgcn_readfirstlane(
+        (int)(ra.lds0 + (uint32_t)(R::B_OFF + (x & (kBSlots - 1)) * R::B_BYTES)));
+  };
+  auto next3 = [](int i) { return i == kASlots - 1 ? 0 : i + 1; };
 
-  // prologue: A block 0, B stages 0 and 1, then A block 1 and B stage 2
-  if (masked && nb == 1) mask_lanes<BM, BN, true, true>(L, wave, lane, kin_last);
-  dma_all<BM, BN, 1>(ra.a_blk(0), L);
-  dma_all<BM, BN, 2>(ra.b_stg(0), L);
-  if (masked && nb == 1) mask_lanes<BM, BN, false, true>(L, wave, lane, kin_last - kSK);
-  dma_all<BM, BN, 2>(ra.b_stg(1), L);
+  // prologue: A block 0 and B stages 0, 1, then A block 1 and B stages 2, 3
+  if (masked && nb == 1) mask_a_lanes<BM, BN>(L, wave, lane, kin_last);
+  dma_all<BM, BN, 1>(a_dma(ra.a0, 0, kOobOffset), L);
+  dma_all<BM, BN, 2>(b_dma(ra.b0, 0), L);
+  dma_all<BM, BN, 2>(b_dma(ra.b0 + ra.b_step, 1), L);
   if (nb > 1) {
-    if (masked && nb == 2) mask_lanes<BM, BN, true, true>(L, wave, lane, kin_last);
-    dma_all<BM, BN, 1>(ra.a_blk(1), L);
-    dma_all<BM, BN, 2>(ra.b_stg(2), L);
-    wait_vmem_at_most<R::APB + R::BPW>();
+    if (masked && nb == 2) mask_a_lanes<BM, BN>(L, wave, lane, kin_last);
+    dma_all<BM, BN, 1>(a_dma(ra.a0 + kBK * 2, 1, kOobOffset), L);
+    dma_all<BM, BN, 2>(b_dma(ra.b0 + 2 * ra.b_step, 2), L);
+    dma_all<BM, BN, 2>(b_dma(ra.b0 + 3 * ra.b_step, 3), L);
+    wait_vmem_at_most<R::APB + 2 * R::BPW>();
   } else {
     wait_vmem_at_most<0>();
   }
@@ -487,41 +513,47 @@ __device__ __forceinline__ void main_loop_ring(const RingAddr<BM, BN>& ra, int n
 
   Frags<BM, BN> f0, f1;
   {
-    uint32_t b_base[Tile<BM, BN>::FN];
-    const uint32_t bs = ra.b_slot(0);
+    uint32_t b_base[T::FN];
+    const uint32_t bs = b_slot(0);
 #pragma unroll
-    for (int j = 0; j < Tile<BM, BN>::FN; ++j) b_base[j] = bs + o.b_rd[0][j];
-    const uint32_t as = ra.a_slot(0) + o.a_rd[0];
+    for (int j = 0; j < T::FN; ++j) b_base[j] = bs + o.b_rd[j];
+    const uint32_t as = a_slot(0) + o.a_rd[0];
     // same order as the reads issued by the loop's last step, so that the
     // first MFMAs wait only for their own operands on either path into the loop
 #pragma unroll
-    for (int t = 0; t < Tile<BM, BN>::FM + Tile<BM, BN>::FN; ++t) {
+    for (int t = 0; t < T::FM + T::FN; ++t) {
       read_item<BM, BN>(t, as, b_base, f0);
       __builtin_amdgcn_sched_barrier(0);
     }
   }
+  // carried state: A slots of blocks b, b+1, b+2; addresses of A block b+2 and
+  // of B stage x0+4
+  int sa0 = 0, sa1 = 1, sa2 = 2;
+  uint64_t a_addr = ra.a0 + 2 * kBK * 2;
+  uint64_t b_addr = ra.b0 + 4 * ra.b_step;
   for (int b = 0; b < nb; ++b) {
     const int x0 = 2 * b;
-    const uint32_t as = ra.a_slot(b);
-    if (masked && b == nb - 2) mask_lanes<BM, BN, false, true>(L, wave, lane, kin_last - kSK);
-    ring_step<BM, BN, 2, 0, BQ>(acc, f0, f1, as + o.a_rd[1], ra.b_slot(x0), 1, o, x0 + 3 < nst,
-                                ra.b_stg(x0 + 3), L);
-    if (masked && b == nb - 3) mask_lanes<BM, BN, true, true>(L, wave, lane, kin_last);
+    if (masked && b == nb - 3) mask_a_lanes<BM, BN>(L, wave, lane, kin_last);
     {
-      const SlotDma d = ra.a_blk(b + 2);
-      const bool on = b + 2 < nb;
-      const uint32_t bs = ra.b_slot(x0 + 1);
-      ring_step<BM, BN, 1, 0, AH>(acc, f1, f0, as + o.a_rd[2], bs, 0, o, on, d, L);
-      ring_step<BM, BN, 1, AH, 2 * AH>(acc, f0, f1, as + o.a_rd[3], bs, 1, o, on, d, L);
-      if (on) wait_vmem_at_most<R::APB>();
-      else wait_vmem_at_most<0>();
+      // a block past K is loaded with an empty range: all lanes read zeros
+      // and nothing is fetched, so the loop needs no branches
+      const SlotDma da = a_dma(a_addr, sa2, b + 2 < nb ? (uint32_t)kOobOffset : 0u);
+      ring_step<BM, BN, 1>(acc, f0, f1, a_slot(sa0) + o.a_rd[1], b_slot(x0 + 1), o, da, da, L);
     }
+    wait_vmem_at_most<R::APB>();
     wait_lds_all();
     __syncthreads();
-    ring_step<BM, BN, 2, 0, BQ>(acc, f1, f0, ra.a_slot(b + 1) + o.a_rd[0], ra.b_slot(x0 + 2), 0, o,
-                                x0 + 4 < nst, ra.b_stg(x0 + 4), L);
+    ring_step<BM, BN, 2>(acc, f1, f0, a_slot(sa1) + o.a_rd[0], b_slot(x0 + 2), o, b_dma(b_addr, x0 + 4),
+                         b_dma(b_addr + ra.b_step, x0 + 5), L);
+    sa0 = sa1;
+    sa1 = sa2;
+    sa2 = next3(sa2);
+    a_addr += kBK * 2;
+    b_addr += 2 * ra.b_step;
   }
-  // the ring's next user starts with a fresh prologue
+  // the last blocks' empty-range loads still write zeros into the ring: let
+  // them land before the next task's prologue loads into the same slots
+  wait_vmem_at_most<0>();
   wait_lds_all();
   __syncthreads();
 }
@@ -529,8 +561,7 @@ __device__ __forceinline__ void main_loop_ring(const RingAddr<BM, BN>& ra, int n
 // ---- main loop, general path: element loads staged in registers ---------------------------
 template <int BM, int BN>
 __device__ __forceinline__ void main_loop_staged(const GemmParams& p, uint16_t* smem, int64_t m0,
-                                                 int64_t n0, int kt0, int kt1, int tid,
-                                                 f32x16 (&acc)[Tile<BM, BN>::FM][Tile<BM, BN>::FN]) {
+                                                 int64_t n0, int kt0, int kt1, int tid, Acc<BM, BN>& acc) {
   using T = Tile<BM, BN>;
   const int lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
@@ -554,7 +585,7 @@ __device__ __forceinline__ void main_loop_staged(const GemmParams& p, uint16_t* 
 #pragma unroll
     for (int i = 0; i < T::A_CH; ++i) {
       const int q = tid + kThreads * i;
-      *reinterpret_cast<u32x4*>(As + a_off<64>(q >> 3, q & 7)) = ra[i];
+      *reinterpret_cast<u32x4*>(As + a_off(q >> 3, q & 7)) = ra[i];
     }
 #pragma unroll
     for (int i = 0; i < T::B_CH; ++i) {
@@ -571,9 +602,9 @@ __device__ __forceinline__ void main_loop_staged(const GemmParams& p, uint16_t* 
     if (more) load_blocks(kt + 1);
     const uint16_t* As = smem + buf * (T::A_ELEMS + T::B_ELEMS);
 #pragma unroll
-    for (int ks = 0; ks < kBK / 16; ++ks) {
+    for (int ks = 0; ks < kBK / 32; ++ks) {
       Frags<BM, BN> f;
-      load_frags<BM, BN, 64>(As, As + T::A_ELEMS, wm, wn, lane, ks, f);
+      load_frags<BM, BN>(As, As + T::A_ELEMS, wm, wn, lane, ks, 32 * ks, f);
       mma_step<BM, BN>(f, acc);
     }
     if (more) store_blocks(buf ^ 1);
@@ -582,59 +613,48 @@ __device__ __forceinline__ void main_loop_staged(const GemmParams& p, uint16_t* 
 }
 
 // ---- epilogue ---------------------------------------------------------------------------------
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
-
+// Fragment (i, j) of the wave: lane l holds row 16i + l%16 and columns
+// 16j + 4*(l/16) .. +3 of the wave's sub-block.
 template <int BM, int BN, bool OUT_BF16>
-__device__ __forceinline__ void store_tile(const GemmParams& p,
-                                           const f32x16 (&acc)[Tile<BM, BN>::FM][Tile<BM, BN>::FN],
-                                           int64_t m0, int64_t n0, int64_t lstride, int wm, int wn,
-                                           int lane, bool fast) {
+__device__ __forceinline__ void store_tile(const GemmParams& p, const Acc<BM, BN>& acc, int64_t m0, int64_t n0,
+                                           int64_t lstride, int wm, int wn, int lane, bool fast) {
   using T = Tile<BM, BN>;
   typedef typename std::conditional<OUT_BF16, __bf16, float>::type OutT;
   OutT* out = reinterpret_cast<OutT*>(p.out) + lstride;
-  const int col_lane = 4 * (lane >> 5);
+  const int64_t r0 = m0 + wm * T::WTM + (lane & 15);
+  const int64_t c0 = n0 + wn * T::WTN + 4 * (lane >> 4);
   if (fast) {
     // whole block inside C and 4-element aligned rows: no checks
 #pragma unroll
     for (int i = 0; i < T::FM; ++i) {
-      OutT* row = out + (m0 + wm * T::WTM + i * 32 + (lane & 31)) * p.ldo + n0 + wn * T::WTN + col_lane;
+      OutT* row = out + (r0 + i * 16) * p.ldo + c0;
 #pragma unroll
       for (int j = 0; j < T::FN; ++j) {
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          OutT* dst = row + j * 32 + q * 8;
-          if (OUT_BF16) {
-            bf16x4 v = {(__bf16)acc[i][j][4 * q], (__bf16)acc[i][j][4 * q + 1],
-                        (__bf16)acc[i][j][4 * q + 2], (__bf16)acc[i][j][4 * q + 3]};
-            *reinterpret_cast<bf16x4*>(dst) = v;
-          } else {
-            f32x4 v = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
-            *reinterpret_cast<f32x4*>(dst) = v;
-          }
+        if (OUT_BF16) {
+          bf16x4 v = {(__bf16)acc[i][j][0], (__bf16)acc[i][j][1], (__bf16)acc[i][j][2], (__bf16)acc[i][j][3]};
+          *reinterpret_cast<bf16x4*>(row + j * 16) = v;
+        } else {
+          *reinterpret_cast<f32x4*>(row + j * 16) = acc[i][j];
         }
-        // keep the scheduler from converting every accumulator before storing any
-        if (OUT_BF16) __builtin_amdgcn_sched_barrier(0);
       }
+      // keep the scheduler from converting every accumulator before storing any
+      if (OUT_BF16) __builtin_amdgcn_sched_barrier(0);
     }
     return;
   }
 #pragma unroll
   for (int i = 0; i < T::FM; ++i) {
-    const int64_t r = m0 + wm * T::WTM + i * 32 + (lane & 31);
+    const int64_t r = r0 + i * 16;
     if (r >= p.M) continue;
     OutT* row = out + r * p.ldo;
 #pragma unroll
     for (int j = 0; j < T::FN; ++j) {
+      const int64_t c = c0 + j * 16;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int64_t c = n0 + wn * T::WTN + j * 32 + q * 8 + col_lane;
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          if (c + e < p.N) row[c + e] = (OutT)acc[i][j][4 * q + e];
-      }
-      if (OUT_BF16) __builtin_amdgcn_sched_barrier(0);
+      for (int e = 0; e < 4; ++e)
+        if (c + e < p.N) row[c + e] = (OutT)acc[i][j][e];
     }
+    if (OUT_BF16) __builtin_amdgcn_sched_barrier(0);
   }
 }
 
@@ -642,7 +662,7 @@ template <int BM, int BN, bool OUT_BF16, bool VEC>
 __global__ __launch_bounds__(kThreads, 1) void sfc_gemm_kernel(GemmParams p) {
   using T = Tile<BM, BN>;
   static_assert(T::A_CH >= 1 && T::B_CH >= 1, "tile too small for 256 threads");
-  // fast path: the ring of stage slots; general path: two 64-deep blocks
+  // fast path: the rings of A block and B stage slots; general path: two 64-deep blocks
   constexpr int kSmem = VEC ? Ring<BM, BN>::ELEMS : 2 * (T::A_ELEMS + T::B_ELEMS);
   __shared__ __attribute__((aligned(16))) uint16_t smem[kSmem];
 
@@ -687,34 +707,31 @@ __global__ __launch_bounds__(kThreads, 1) void sfc_gemm_kernel(GemmParams p) {
     const int kt0 = (int)((unsigned)layer * (unsigned)p.nk / (unsigned)p.layers);
     const int kt1 = (int)((unsigned)(layer + 1) * (unsigned)p.nk / (unsigned)p.layers);
 
-    f32x16 acc[T::FM][T::FN];
+    Acc<BM, BN> acc;
 #pragma unroll
     for (int i = 0; i < T::FM; ++i)
 #pragma unroll
-      for (int j = 0; j < T::FN; ++j)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+      for (int j = 0; j < T::FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     if (kt0 < kt1) {
       if constexpr (VEC) {
-        // a last block that runs past K is loaded with per-lane masks
-        const int64_t kin_last = p.K - (int64_t)(kt1 - 1) * kBK;
+        const int64_t k0 = (int64_t)kt0 * kBK;
         RingLanes<BM, BN> L;
         ring_lanes<BM, BN>(p, m0, n0, wave, lane_t, L);
-        RingAddr<BM, BN> ra;
-        ra.a0 = reinterpret_cast<uint64_t>(p.A + m0 * p.lda + (int64_t)kt0 * kBK) - kBias;
-        ra.b0 = reinterpret_cast<uint64_t>(p.B + (int64_t)kt0 * kBK * p.ldb + n0) - kBias;
+        RingAddr ra;
+        ra.a0 = reinterpret_cast<uint64_t>(p.A + m0 * p.lda + k0) - kBias;
+        ra.b0 = reinterpret_cast<uint64_t>(p.B + k0 * p.ldb + n0) - kBias;
         ra.b_step = (uint64_t)kSK * (uint64_t)p.ldb * 2;
+        ra.b_rows = (int)(p.K - k0);
+        ra.ldb2 = (int)(p.ldb * 2);
         ra.lds0 = lds_addr(smem);
         ra.wave = wave;
-        main_loop_ring<BM, BN>(ra, kt1 - kt0, kin_last, ro, L, lane_t, acc);
+        main_loop_ring<BM, BN>(ra, kt1 - kt0, p.K - (int64_t)(kt1 - 1) * kBK, ro, L, lane_t, acc);
       } else {
         main_loop_staged<BM, BN>(p, smem, m0, n0, kt0, kt1, tid, acc);
       }
     }
 
-    // Epilogue.  Accumulator element e of fragment (i, j) is row lane%32 and
-    // column 8*(e/4) + 4*(lane/32) + e%4 of that 32x32 fragment.
     const int64_t lstride = p.out_layer_stride * layer;
     const bool interior = m0 + BM <= p.M && n0 + BN <= p.N;
     store_tile<BM, BN, OUT_BF16>(p, acc, m0, n0, lstride, wm, wn, lane_t, interior && vec_store);
