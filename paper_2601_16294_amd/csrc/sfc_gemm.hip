@@ -294,9 +294,10 @@ __device__ __forceinline__ void mask_a_lanes(RingLanes<BM, BN>& L, int wave, int
     if (a_load_k(wave, R::APB, j, lane) >= kin) L.a_voff[j] = kOobOffset;
 }
 
-// Per-lane LDS byte offsets of the fragment reads within a slot: A fragment i
-// of step ks at a_rd[ks] + i*2048; the two halves of B fragment j at b_rd[j]
-// and b_rd[j] + 8*BN.
+// Per-lane LDS byte offsets of the fragment reads: A fragment i of step ks at
+// a_rd[ks] + i*2048 within its slot; the two halves of B fragment j at
+// b_rd[j] and b_rd[j] + 8*BN in B slot 0 (LDS byte addresses; slot s adds
+// s times the slot size, an immediate offset of the read).
 template <int BM, int BN>
 struct ReadOffsets {
   uint32_t a_rd[2];
@@ -304,26 +305,30 @@ struct ReadOffsets {
 };
 
 template <int BM, int BN>
-__device__ __forceinline__ void read_offsets(int wm, int wn, int lane, ReadOffsets<BM, BN>& o) {
+__device__ __forceinline__ void read_offsets(int wm, int wn, int lane, uint32_t b_ring, ReadOffsets<BM, BN>& o) {
   using T = Tile<BM, BN>;
 #pragma unroll
   for (int ks = 0; ks < 2; ++ks) o.a_rd[ks] = (uint32_t)(a_frag_off(wm * T::WTM, lane, ks) * 2);
 #pragma unroll
-  for (int j = 0; j < T::FN; ++j) o.b_rd[j] = (uint32_t)(b_frag_off<BN>(wn * T::WTN, lane, 0, j) * 2);
+  for (int j = 0; j < T::FN; ++j) o.b_rd[j] = b_ring + (uint32_t)(b_frag_off<BN>(wn * T::WTN, lane, 0, j) * 2);
 }
 
 // Read item t of a step, in the order the next step's MFMAs consume them:
 // A0, B0, B1, .., B(FN-1), A1, .., A(FM-1).
 template <int BM, int BN>
-__device__ __forceinline__ void read_item(int t, uint32_t a_base, const uint32_t* b_base, Frags<BM, BN>& f) {
+__device__ __forceinline__ void read_item(int t, uint32_t a_base, uint32_t b_slot, const uint32_t* b_rd,
+                                          Frags<BM, BN>& f) {
   using T = Tile<BM, BN>;
   if (t == 0 || t > T::FN) {
     const int i = t == 0 ? 0 : t - T::FN;
     f.a[i] = *(lds_bf16x8*)(uintptr_t)(a_base + (uint32_t)(i * 16 * kBK * 2));
   } else {
     const int j = t - 1;
-    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(uintptr_t)b_base[j]);
-    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(uintptr_t)(b_base[j] + 8 * BN));
+    // the slot offset is added here, beside the reads, rather than for all
+    // fragments at once at the start of a step
+    const uint32_t b_addr = b_slot + b_rd[j];
+    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(uintptr_t)b_addr);
+    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(uintptr_t)(b_addr + 8 * BN));
     const i16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
     f.b[j] = __builtin_bit_cast(bf16x8, v);
   }
@@ -356,11 +361,12 @@ __device__ __forceinline__ void dma_all(const SlotDma& d, const RingLanes<BM, BN
 
 // One group of a step: MFMA g, then the reads and the load pair that fall on g.
 template <int BM, int BN, int OP, int g, int... t>
-__device__ __forceinline__ void group_reads(uint32_t a_base, const uint32_t* b_base, Frags<BM, BN>& nxt,
+__device__ __forceinline__ void group_reads(uint32_t a_base, uint32_t b_slot, const uint32_t* b_rd,
+                                            Frags<BM, BN>& nxt,
                                             std::integer_sequence<int, t...>) {
   using T = Tile<BM, BN>;
   constexpr int G = T::FM * T::FN, NI = T::FM + T::FN;
-  ((void)((t * G) / NI == g ? (read_item<BM, BN>(t, a_base, b_base, nxt), 0) : 0), ...);
+  ((void)((t * G) / NI == g ? (read_item<BM, BN>(t, a_base, b_slot, b_rd, nxt), 0) : 0), ...);
 }
 
 template <int BM, int BN, int OP>
@@ -370,12 +376,26 @@ struct StepLoads {
   static constexpr int NP = NP0 + NP1;
 };
 
+// Group of load pair q: evenly spread, moved forward past groups that already
+// issue fragment reads (each group has room for about three instructions
+// beside its MFMA before the matrix core waits).
+template <int BM, int BN, int OP>
+constexpr int load_group(int q) {
+  using T = Tile<BM, BN>;
+  constexpr int G = T::FM * T::FN, NI = T::FM + T::FN;
+  int g = ((2 * q + 1) * G) / (2 * StepLoads<BM, BN, OP>::NP);
+  for (;;) {
+    bool busy = false;
+    for (int t = 0; t < NI; ++t) busy = busy || (t * G) / NI == g;
+    if (!busy || g == G - 1) return g;
+    ++g;
+  }
+}
+
 template <int BM, int BN, int OP, int g, int q>
 __device__ __forceinline__ void group_load(const SlotDma& d0, const SlotDma& d1, const RingLanes<BM, BN>& L) {
-  using T = Tile<BM, BN>;
   using S = StepLoads<BM, BN, OP>;
-  constexpr int G = T::FM * T::FN;
-  if constexpr (((2 * q + 1) * G) / (2 * S::NP) == g) {
+  if constexpr (load_group<BM, BN, OP>(q) == g) {
     if constexpr (q < S::NP0) dma_pair<BM, BN, OP, q>(d0, L);
     else dma_pair<BM, BN, OP, q - S::NP0>(d1, L);
   }
@@ -389,22 +409,22 @@ __device__ __forceinline__ void group_loads(const SlotDma& d0, const SlotDma& d1
 
 template <int BM, int BN, int OP, int g>
 __device__ __forceinline__ void ring_group(Acc<BM, BN>& acc, const Frags<BM, BN>& cur, Frags<BM, BN>& nxt,
-                                           uint32_t a_base, const uint32_t* b_base, const SlotDma& d0,
+                                           uint32_t a_base, uint32_t b_slot, const uint32_t* b_rd, const SlotDma& d0,
                                            const SlotDma& d1, const RingLanes<BM, BN>& L) {
   using T = Tile<BM, BN>;
   constexpr int i = g / T::FN, j = g % T::FN;
   acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(cur.b[j], cur.a[i], acc[i][j], 0, 0, 0);
-  group_reads<BM, BN, OP, g>(a_base, b_base, nxt, std::make_integer_sequence<int, T::FM + T::FN>{});
+  group_reads<BM, BN, OP, g>(a_base, b_slot, b_rd, nxt, std::make_integer_sequence<int, T::FM + T::FN>{});
   group_loads<BM, BN, OP, g>(d0, d1, L, std::make_integer_sequence<int, StepLoads<BM, BN, OP>::NP>{});
   __builtin_amdgcn_sched_barrier(0);
 }
 
 template <int BM, int BN, int OP, int... g>
 __device__ __forceinline__ void ring_groups(Acc<BM, BN>& acc, const Frags<BM, BN>& cur, Frags<BM, BN>& nxt,
-                                            uint32_t a_base, const uint32_t* b_base, const SlotDma& d0,
+                                            uint32_t a_base, uint32_t b_slot, const uint32_t* b_rd, const SlotDma& d0,
                                             const SlotDma& d1, const RingLanes<BM, BN>& L,
                                             std::integer_sequence<int, g...>) {
-  (ring_group<BM, BN, OP, g>(acc, cur, nxt, a_base, b_base, d0, d1, L), ...);
+  (ring_group<BM, BN, OP, g>(acc, cur, nxt, a_base, b_slot, b_rd, d0, d1, L), ...);
 }
 
 // One 32-deep step with a fixed instruction order: group g issues MFMA g of
@@ -419,10 +439,7 @@ __device__ __forceinline__ void ring_step(Acc<BM, BN>& acc, const Frags<BM, BN>&
                                           uint32_t a_base, uint32_t b_slot, const ReadOffsets<BM, BN>& o,
                                           const SlotDma& d0, const SlotDma& d1, const RingLanes<BM, BN>& L) {
   using T = Tile<BM, BN>;
-  uint32_t b_base[T::FN];
-#pragma unroll
-  for (int j = 0; j < T::FN; ++j) b_base[j] = b_slot + o.b_rd[j];
-  ring_groups<BM, BN, OP>(acc, cur, nxt, a_base, b_base, d0, d1, L,
+  ring_groups<BM, BN, OP>(acc, cur, nxt, a_base, b_slot, o.b_rd, d0, d1, L,
                           std::make_integer_sequence<int, T::FM * T::FN>{});
 }
 
@@ -431,8 +448,8 @@ __device__ __forceinline__ void ring_step(Acc<BM, BN>& acc, const Frags<BM, BN>&
 struct RingAddr {
   uint64_t a0, b0;           // byte address of the first block's A origin and B origin, minus kBias
   uint64_t b_step;           // bytes between consecutive B stages (32 rows of B)
-  int b_rows;                // rows of B from the first stage's origin to row K
-  int ldb2;                  // bytes per row of B
+  int x_part;                // first B stage that is not wholly before row K
+  uint32_t lim_part;         // its num_records: its rows before K, plus the bias
   uint32_t lds0;             // LDS byte address of the ring
   int wave;
 };
@@ -440,8 +457,7 @@ struct RingAddr {
 // num_records of B stage x: rows at or past K fall outside and read zeros (a
 // stage wholly past K reads nothing from memory)
 __device__ __forceinline__ uint32_t b_stage_limit(const RingAddr& ra, int x) {
-  const int rows = min(max(ra.b_rows - x * kSK, 0), kSK);
-  return rows == kSK ? (uint32_t)kOobOffset : (uint32_t)(rows * ra.ldb2 + kBias);
+  return x < ra.x_part ? (uint32_t)kOobOffset : x == ra.x_part ? ra.lim_part : (uint32_t)kBias;
 }
 
 // The K loop of one task over nb 64-deep blocks.  Block b = A block b and B
@@ -490,8 +506,7 @@ __device__ __forceinline__ void main_loop_ring(const RingAddr& ra, int nb, int64
     return (uint32_t)__builtin_amdgcn_readfirstlane((int)(ra.lds0 + (uint32_t)(slot * R::A_BYTES)));
   };
   auto b_slot = [&](int x) {
-    return (uint32_t)__builtin_amdgcn_readfirstlane(
-        (int)(ra.lds0 + (uint32_t)(R::B_OFF + (x & (kBSlots - 1)) * R::B_BYTES)));
+    return (uint32_t)__builtin_amdgcn_readfirstlane((int)((uint32_t)((x & (kBSlots - 1)) * R::B_BYTES)));
   };
   auto next3 = [](int i) { return i == kASlots - 1 ? 0 : i + 1; };
 
@@ -513,19 +528,21 @@ __device__ __forceinline__ void main_loop_ring(const RingAddr& ra, int nb, int64
 
   Frags<BM, BN> f0, f1;
   {
-    uint32_t b_base[T::FN];
-    const uint32_t bs = b_slot(0);
-#pragma unroll
-    for (int j = 0; j < T::FN; ++j) b_base[j] = bs + o.b_rd[j];
     const uint32_t as = a_slot(0) + o.a_rd[0];
+    // B slot 0, as an opaque register value: with a literal 0 the compiler
+    // would keep b_rd[j] + 8*BN in registers across tasks
+    uint32_t bs0;
+    asm volatile("s_mov_b32 %0, 0" : "=s"(bs0));
     // same order as the reads issued by the loop's last step, so that the
     // first MFMAs wait only for their own operands on either path into the loop
 #pragma unroll
     for (int t = 0; t < T::FM + T::FN; ++t) {
-      read_item<BM, BN>(t, as, b_base, f0);
+      read_item<BM, BN>(t, as, bs0, o.b_rd, f0);
       __builtin_amdgcn_sched_barrier(0);
     }
   }
+  // block whose A loads get the K mask (none when K is a multiple of 64)
+  const int mask_b = __builtin_amdgcn_readfirstlane(masked ? nb - 3 : -1);
   // carried state: A slots of blocks b, b+1, b+2; addresses of A block b+2 and
   // of B stage x0+4
   int sa0 = 0, sa1 = 1, sa2 = 2;
@@ -533,7 +550,7 @@ __device__ __forceinline__ void main_loop_ring(const RingAddr& ra, int nb, int64
   uint64_t b_addr = ra.b0 + 4 * ra.b_step;
   for (int b = 0; b < nb; ++b) {
     const int x0 = 2 * b;
-    if (masked && b == nb - 3) mask_a_lanes<BM, BN>(L, wave, lane, kin_last);
+    if (b == mask_b) mask_a_lanes<BM, BN>(L, wave, lane, kin_last);
     {
       // a block past K is loaded with an empty range: all lanes read zeros
       // and nothing is fetched, so the loop needs no branches
@@ -671,7 +688,7 @@ __global__ __launch_bounds__(kThreads, 1) void sfc_gemm_kernel(GemmParams p) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
   ReadOffsets<BM, BN> ro;
-  if constexpr (VEC) read_offsets<BM, BN>(wm, wn, lane, ro);
+  if constexpr (VEC) read_offsets<BM, BN>(wm, wn, lane, lds_addr(smem) + (uint32_t)Ring<BM, BN>::B_OFF, ro);
 
   const int P = gridDim.x;
   const int rank = xcd_rank(blockIdx.x, P);
@@ -722,8 +739,11 @@ __global__ __launch_bounds__(kThreads, 1) void sfc_gemm_kernel(GemmParams p) {
         ra.a0 = reinterpret_cast<uint64_t>(p.A + m0 * p.lda + k0) - kBias;
         ra.b0 = reinterpret_cast<uint64_t>(p.B + k0 * p.ldb + n0) - kBias;
         ra.b_step = (uint64_t)kSK * (uint64_t)p.ldb * 2;
-        ra.b_rows = (int)(p.K - k0);
-        ra.ldb2 = (int)(p.ldb * 2);
+        {
+          const int b_rows = (int)(p.K - k0);   // rows of B from the task's first stage to row K
+          ra.x_part = b_rows / kSK;
+          ra.lim_part = (uint32_t)((b_rows % kSK) * (int)(p.ldb * 2) + kBias);
+        }
         ra.lds0 = lds_addr(smem);
         ra.wave = wave;
         main_loop_ring<BM, BN>(ra, kt1 - kt0, p.K - (int64_t)(kt1 - 1) * kBK, ro, L, lane_t, acc);
