@@ -294,6 +294,15 @@ __device__ __forceinline__ void mask_a_lanes(RingLanes<BM, BN>& L, int wave, int
     if (a_load_k(wave, R::APB, j, lane) >= kin) L.a_voff[j] = kOobOffset;
 }
 
+// The same without a branch: masks only when `on` (wave-uniform).
+template <int BM, int BN>
+__device__ __forceinline__ void mask_a_lanes_if(RingLanes<BM, BN>& L, int wave, int lane, int64_t kin, bool on) {
+  using R = Ring<BM, BN>;
+#pragma unroll
+  for (int j = 0; j < R::APB; ++j)
+    L.a_voff[j] = (on && a_load_k(wave, R::APB, j, lane) >= kin) ? kOobOffset : L.a_voff[j];
+}
+
 // Per-lane LDS byte offsets of the fragment reads: A fragment i of step ks at
 // a_rd[ks] + i*2048 within its slot; the two halves of B fragment j at
 // b_rd[j] and b_rd[j] + 8*BN in B slot 0 (LDS byte addresses; slot s adds
@@ -359,87 +368,162 @@ __device__ __forceinline__ void dma_all(const SlotDma& d, const RingLanes<BM, BN
   }(std::make_integer_sequence<int, (OP == 1 ? R::APB : R::BPW) / 2>{});
 }
 
-// One group of a step: MFMA g, then the reads and the load pair that fall on g.
-template <int BM, int BN, int OP, int g, int... t>
-__device__ __forceinline__ void group_reads(uint32_t a_base, uint32_t b_slot, const uint32_t* b_rd,
-                                            Frags<BM, BN>& nxt,
-                                            std::integer_sequence<int, t...>) {
-  using T = Tile<BM, BN>;
-  constexpr int G = T::FM * T::FN, NI = T::FM + T::FN;
-  ((void)((t * G) / NI == g ? (read_item<BM, BN>(t, a_base, b_slot, b_rd, nxt), 0) : 0), ...);
-}
-
+// Instruction plan of one 32-deep step: FM*FN groups, each one MFMA of the
+// current fragments plus at most one fragment read for the next step and at
+// most one load operation.  With one wave per SIMD a wave issues one
+// instruction every 4 cycles, so a 16-cycle MFMA hides three others; two LDS
+// reads in one group already cost extra cycles (both measured on gfx950).
+//   reads:  A0, B0 low, B0 high, B1 low, .., B(FN-1) high, A1, .., A(FM-1)
+//           (the order the next step's MFMAs consume them), spread evenly;
+//   loads:  each load pair becomes three operations (set M0, load, load) in
+//           consecutive groups from evenly spaced starting groups, so that the
+//           MFMA between M0 and the first load covers the wait M0 needs.
 template <int BM, int BN, int OP>
-struct StepLoads {
+struct StepPlan {
+  using T = Tile<BM, BN>;
+  static constexpr int G = T::FM * T::FN;
+  static constexpr int NR = T::FM + 2 * T::FN;
   static constexpr int NP0 = OP == 1 ? Ring<BM, BN>::APB / 2 : Ring<BM, BN>::BPW / 2;   // pairs from d0
   static constexpr int NP1 = OP == 1 ? 0 : Ring<BM, BN>::BPW / 2;                      // pairs from d1
   static constexpr int NP = NP0 + NP1;
+  static constexpr int ND = 3 * NP;
+  static constexpr int read_group(int r) { return (r * G) / NR; }
+  static constexpr int dma_group(int o) {
+    int g = -1;
+    for (int i = 0; i <= o; ++i) {
+      const int start = ((2 * (i / 3) + 1) * G) / (2 * NP) - 1 + i % 3;
+      g = g + 1 > start ? g + 1 : start;
+    }
+    return g;
+  }
+  // groups that issue neither a read nor a load operation (nor, in the A
+  // step, one of the K-mask selects of the first APB groups)
+  static constexpr bool busy(int g) {
+    if (OP == 1 && g < Ring<BM, BN>::APB) return true;
+    for (int r = 0; r < NR; ++r)
+      if (read_group(r) == g) return true;
+    for (int o = 0; o < ND; ++o)
+      if (dma_group(o) == g) return true;
+    return false;
+  }
+  // group of scalar stage s of ns: spread over the free groups
+  static constexpr int stage_group(int s, int ns) {
+    int nfree = 0;
+    for (int g = 0; g < G; ++g) nfree += busy(g) ? 0 : 1;
+    if (nfree >= ns) {
+      const int want = (s * nfree) / ns;
+      int k = 0;
+      for (int g = 0; g < G; ++g) {
+        if (busy(g)) continue;
+        if (k == want) return g;
+        ++k;
+      }
+    }
+    return (s * G) / ns;
+  }
+  static_assert(NR <= G, "one read per group");
+  static_assert(ND == 0 || dma_group(ND - 1) < G, "loads fit in the step");
 };
 
-// Group of load pair q: evenly spread, moved forward past groups that already
-// issue fragment reads (each group has room for about three instructions
-// beside its MFMA before the matrix core waits).
-template <int BM, int BN, int OP>
-constexpr int load_group(int q) {
+// Per-step state of the split B reads: address and low half of each fragment.
+template <int BM, int BN>
+struct BReads {
+  uint32_t addr[Tile<BM, BN>::FN];
+  i16x4 lo[Tile<BM, BN>::FN];
+};
+
+template <int BM, int BN, int OP, int r>
+__device__ __forceinline__ void step_read(uint32_t a_base, uint32_t b_slot, const uint32_t* b_rd, BReads<BM, BN>& br,
+                                          Frags<BM, BN>& nxt) {
   using T = Tile<BM, BN>;
-  constexpr int G = T::FM * T::FN, NI = T::FM + T::FN;
-  int g = ((2 * q + 1) * G) / (2 * StepLoads<BM, BN, OP>::NP);
-  for (;;) {
-    bool busy = false;
-    for (int t = 0; t < NI; ++t) busy = busy || (t * G) / NI == g;
-    if (!busy || g == G - 1) return g;
-    ++g;
+  if constexpr (r == 0 || r > 2 * T::FN) {
+    constexpr int i = r == 0 ? 0 : r - 2 * T::FN;
+    nxt.a[i] = *(lds_bf16x8*)(uintptr_t)(a_base + (uint32_t)(i * 16 * kBK * 2));
+  } else if constexpr ((r - 1) % 2 == 0) {
+    constexpr int j = (r - 1) / 2;
+    br.addr[j] = b_slot + b_rd[j];
+    br.lo[j] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(uintptr_t)br.addr[j]);
+  } else {
+    constexpr int j = (r - 1) / 2;
+    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(uintptr_t)(br.addr[j] + 8 * BN));
+    const i16x4 lo = br.lo[j];
+    const i16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    nxt.b[j] = __builtin_bit_cast(bf16x8, v);
   }
 }
 
-template <int BM, int BN, int OP, int g, int q>
-__device__ __forceinline__ void group_load(const SlotDma& d0, const SlotDma& d1, const RingLanes<BM, BN>& L) {
-  using S = StepLoads<BM, BN, OP>;
-  if constexpr (load_group<BM, BN, OP>(q) == g) {
-    if constexpr (q < S::NP0) dma_pair<BM, BN, OP, q>(d0, L);
-    else dma_pair<BM, BN, OP, q - S::NP0>(d1, L);
+template <int BM, int BN, int OP, int g, int... r>
+__device__ __forceinline__ void group_reads(uint32_t a_base, uint32_t b_slot, const uint32_t* b_rd,
+                                            BReads<BM, BN>& br, Frags<BM, BN>& nxt, std::integer_sequence<int, r...>) {
+  using P = StepPlan<BM, BN, OP>;
+  ((void)(P::read_group(r) == g ? (step_read<BM, BN, OP, r>(a_base, b_slot, b_rd, br, nxt), 0) : 0), ...);
+}
+
+// Load operation o of a step: o = 3q + k for load pair q (k 0: set M0, k 1
+// and 2: the pair's loads).
+template <int BM, int BN, int OP, int o>
+__device__ __forceinline__ void step_dma(const SlotDma& d0, const SlotDma& d1, const RingLanes<BM, BN>& L) {
+  using P = StepPlan<BM, BN, OP>;
+  constexpr int q = o / 3, k = o % 3;
+  constexpr bool first = q < P::NP0;
+  constexpr int qq = first ? q : q - P::NP0;
+  const SlotDma& d = first ? d0 : d1;
+  constexpr int j = 2 * qq + (k == 2 ? 1 : 0);
+  if constexpr (k == 0) {
+    const uint32_t m0v = OP == 1 ? d.m0 + (uint32_t)((j >> 2) * 4096) : d.m0;
+    asm volatile("s_mov_b32 m0, %0" :: "s"(m0v) : "memory");
+  } else {
+    constexpr int off = OP == 1 ? (j & 3) * 1024 : j * 1024;
+    static_assert(off <= 4095, "instruction offset range");
+    const int v = OP == 1 ? L.a_voff[j] : L.b_voff[j];
+    asm volatile("buffer_load_dwordx4 %0, %1, 0 offen offset:%2 lds" :: "v"(v), "s"(d.rsrc), "n"(off) : "memory");
   }
 }
 
-template <int BM, int BN, int OP, int g, int... q>
-__device__ __forceinline__ void group_loads(const SlotDma& d0, const SlotDma& d1, const RingLanes<BM, BN>& L,
-                                            std::integer_sequence<int, q...>) {
-  (group_load<BM, BN, OP, g, q>(d0, d1, L), ...);
+template <int BM, int BN, int OP, int g, int... o>
+__device__ __forceinline__ void group_dma(const SlotDma& d0, const SlotDma& d1, const RingLanes<BM, BN>& L,
+                                          std::integer_sequence<int, o...>) {
+  using P = StepPlan<BM, BN, OP>;
+  ((void)(P::dma_group(o) == g ? (step_dma<BM, BN, OP, o>(d0, d1, L), 0) : 0), ...);
 }
 
-template <int BM, int BN, int OP, int g>
+template <int BM, int BN, int OP, int g, typename X>
 __device__ __forceinline__ void ring_group(Acc<BM, BN>& acc, const Frags<BM, BN>& cur, Frags<BM, BN>& nxt,
-                                           uint32_t a_base, uint32_t b_slot, const uint32_t* b_rd, const SlotDma& d0,
-                                           const SlotDma& d1, const RingLanes<BM, BN>& L) {
+                                           uint32_t a_base, uint32_t b_slot, const uint32_t* b_rd,
+                                           BReads<BM, BN>& br, const SlotDma& d0, const SlotDma& d1,
+                                           const RingLanes<BM, BN>& L, X& ex) {
   using T = Tile<BM, BN>;
+  using P = StepPlan<BM, BN, OP>;
   constexpr int i = g / T::FN, j = g % T::FN;
   acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(cur.b[j], cur.a[i], acc[i][j], 0, 0, 0);
-  group_reads<BM, BN, OP, g>(a_base, b_slot, b_rd, nxt, std::make_integer_sequence<int, T::FM + T::FN>{});
-  group_loads<BM, BN, OP, g>(d0, d1, L, std::make_integer_sequence<int, StepLoads<BM, BN, OP>::NP>{});
+  group_reads<BM, BN, OP, g>(a_base, b_slot, b_rd, br, nxt, std::make_integer_sequence<int, P::NR>{});
+  group_dma<BM, BN, OP, g>(d0, d1, L, std::make_integer_sequence<int, P::ND>{});
+  ex.template operator()<g>();
   __builtin_amdgcn_sched_barrier(0);
 }
 
-template <int BM, int BN, int OP, int... g>
+template <int BM, int BN, int OP, typename X, int... g>
 __device__ __forceinline__ void ring_groups(Acc<BM, BN>& acc, const Frags<BM, BN>& cur, Frags<BM, BN>& nxt,
-                                            uint32_t a_base, uint32_t b_slot, const uint32_t* b_rd, const SlotDma& d0,
-                                            const SlotDma& d1, const RingLanes<BM, BN>& L,
-                                            std::integer_sequence<int, g...>) {
-  (ring_group<BM, BN, OP, g>(acc, cur, nxt, a_base, b_slot, b_rd, d0, d1, L), ...);
+                                            uint32_t a_base, uint32_t b_slot, const uint32_t* b_rd,
+                                            BReads<BM, BN>& br, const SlotDma& d0, const SlotDma& d1,
+                                            const RingLanes<BM, BN>& L, X& ex, std::integer_sequence<int, g...>) {
+  (ring_group<BM, BN, OP, g>(acc, cur, nxt, a_base, b_slot, b_rd, br, d0, d1, L, ex), ...);
 }
 
-// One 32-deep step with a fixed instruction order: group g issues MFMA g of
-// `cur` (i-major), then the fragment reads of `nxt` that fall on g, then the
-// load pair that falls on g.  Loads: the pairs of an A block d0 (OP 1), or the
-// pairs of two B stages d0 and d1 (OP 2), spread evenly over the groups so
-// that neither the LDS nor the texture path receives a burst.  The groups are
-// generated as straight-line code (a loop this long is not always unrolled,
-// and the accumulators must stay in registers).
-template <int BM, int BN, int OP>
+// One 32-deep step with a fixed instruction order (the plan above): MFMAs of
+// `cur` (i-major), reads of `nxt`, the loads of an A block d0 (OP 1) or of two
+// B stages d0 and d1 (OP 2), and the scalar work `ex` puts on each group
+// (ex.operator()<g>() runs in group g).  The groups are generated as
+// straight-line code (a loop this long is not always unrolled, and the
+// accumulators must stay in registers).
+template <int BM, int BN, int OP, typename X>
 __device__ __forceinline__ void ring_step(Acc<BM, BN>& acc, const Frags<BM, BN>& cur, Frags<BM, BN>& nxt,
                                           uint32_t a_base, uint32_t b_slot, const ReadOffsets<BM, BN>& o,
-                                          const SlotDma& d0, const SlotDma& d1, const RingLanes<BM, BN>& L) {
+                                          const SlotDma& d0, const SlotDma& d1, const RingLanes<BM, BN>& L,
+                                          X&& ex) {
   using T = Tile<BM, BN>;
-  ring_groups<BM, BN, OP>(acc, cur, nxt, a_base, b_slot, o.b_rd, d0, d1, L,
+  BReads<BM, BN> br;
+  ring_groups<BM, BN, OP>(acc, cur, nxt, a_base, b_slot, o.b_rd, br, d0, d1, L, ex,
                           std::make_integer_sequence<int, T::FM * T::FN>{});
 }
 
@@ -470,45 +554,45 @@ __device__ __forceinline__ uint32_t b_stage_limit(const RingAddr& ra, int x) {
 // A block kb lives in A slot kb mod 3, B stage x in B slot x mod 4.  Every load
 // goes into a slot whose last reads were issued before the barrier that
 // precedes the load; the shortest lead from a load to the barrier that
-// publishes it is one step.  The per-block scalar work (descriptors, slot
-// addresses) is carried from block to block so that little of it sits between
-// MFMAs.  The last blocks still issue their loads, for blocks and stages past
-// K, with empty ranges (no memory is read, zeros land in slots that are not
-// read again), so that the loop has no branches around loads or waits.
+// publishes it is one step.  The last blocks still issue their loads, for
+// blocks and stages past K, with empty ranges (no memory is read, zeros land
+// in slots that are not read again), so that the loop has no branches.
+//
+// The scalar bookkeeping (slot addresses, descriptors, limits) is carried from
+// block to block and updated in small pieces on chosen groups of the steps:
+// step 1 builds the B descriptors step 2 loads with; step 2 advances the state
+// to the next block.
 //
 // When the last block runs past K (kin_last < 64): B rows at or past K fall
 // outside the B descriptors' ranges and read zeros; A block nb-1 is loaded with
-// its lanes past K masked (the mask goes on right before those loads, which are
-// the last A loads of the task).
+// its lanes past K masked (selects on the first groups of the step that issues
+// those loads, the last A loads of the task).
 template <int BM, int BN>
 __device__ __forceinline__ void main_loop_ring(const RingAddr& ra, int nb, int64_t kin_last,
                                                const ReadOffsets<BM, BN>& o, RingLanes<BM, BN>& L, int lane,
                                                Acc<BM, BN>& acc) {
   using R = Ring<BM, BN>;
   using T = Tile<BM, BN>;
+  using P1 = StepPlan<BM, BN, 1>;
+  using P2 = StepPlan<BM, BN, 2>;
+  constexpr uint32_t BB = (uint32_t)R::B_BYTES;
+  static_assert((BB & (BB - 1)) == 0, "B slot size is a power of two");
   const int wave = ra.wave;
   const bool masked = kin_last < kBK;
-  const uint32_t a_m0w = (uint32_t)(wave * R::APB * 1024);          // this wave's first A segment
-  const uint32_t b_m0w = (uint32_t)(R::B_OFF + wave * R::BPW * 1024);
+  const uint32_t a_m0w = ra.lds0 + (uint32_t)(wave * R::APB * 1024);            // this wave's segment, A slot 0
+  const uint32_t b_m0w = ra.lds0 + (uint32_t)(R::B_OFF + wave * R::BPW * 1024);  // this wave's segment, B slot 0
   auto a_dma = [&](uint64_t addr, int slot, uint32_t lim) {
     SlotDma d;
     d.rsrc = make_rsrc_addr(addr, lim);
-    d.m0 = ra.lds0 + a_m0w + (uint32_t)(slot * R::A_BYTES);
+    d.m0 = a_m0w + (uint32_t)(slot * R::A_BYTES);
     return d;
   };
   auto b_dma = [&](uint64_t addr, int x) {
     SlotDma d;
     d.rsrc = make_rsrc_addr(addr, b_stage_limit(ra, x));
-    d.m0 = ra.lds0 + b_m0w + (uint32_t)((x & (kBSlots - 1)) * R::B_BYTES);
+    d.m0 = b_m0w + (uint32_t)((x & (kBSlots - 1)) * R::B_BYTES);
     return d;
   };
-  auto a_slot = [&](int slot) {
-    return (uint32_t)__builtin_amdgcn_readfirstlane((int)(ra.lds0 + (uint32_t)(slot * R::A_BYTES)));
-  };
-  auto b_slot = [&](int x) {
-    return (uint32_t)__builtin_amdgcn_readfirstlane((int)((uint32_t)((x & (kBSlots - 1)) * R::B_BYTES)));
-  };
-  auto next3 = [](int i) { return i == kASlots - 1 ? 0 : i + 1; };
 
   // prologue: A block 0 and B stages 0, 1, then A block 1 and B stages 2, 3
   if (masked && nb == 1) mask_a_lanes<BM, BN>(L, wave, lane, kin_last);
@@ -528,7 +612,7 @@ __device__ __forceinline__ void main_loop_ring(const RingAddr& ra, int nb, int64
 
   Frags<BM, BN> f0, f1;
   {
-    const uint32_t as = a_slot(0) + o.a_rd[0];
+    const uint32_t as = ra.lds0 + o.a_rd[0];
     // B slot 0, as an opaque register value: with a literal 0 the compiler
     // would keep b_rd[j] + 8*BN in registers across tasks
     uint32_t bs0;
@@ -541,32 +625,66 @@ __device__ __forceinline__ void main_loop_ring(const RingAddr& ra, int nb, int64
       __builtin_amdgcn_sched_barrier(0);
     }
   }
-  // block whose A loads get the K mask (none when K is a multiple of 64)
-  const int mask_b = __builtin_amdgcn_readfirstlane(masked ? nb - 3 : -1);
-  // carried state: A slots of blocks b, b+1, b+2; addresses of A block b+2 and
-  // of B stage x0+4
-  int sa0 = 0, sa1 = 1, sa2 = 2;
-  uint64_t a_addr = ra.a0 + 2 * kBK * 2;
-  uint64_t b_addr = ra.b0 + 4 * ra.b_step;
+
+  // per-lane K-mask condition of each A load (used on block nb-3, whose step 1
+  // loads A block nb-1; from nb <= 2 on the prologue has masked)
+  bool mk[R::APB];
+#pragma unroll
+  for (int j = 0; j < R::APB; ++j) mk[j] = a_load_k(wave, R::APB, j, lane) >= kin_last;
+  const int mask_b = masked ? nb - 3 : -1;
+
+  // scalar state of block b
+  uint32_t la0 = 0, la1 = R::A_BYTES, la2 = 2 * R::A_BYTES;   // A slots of blocks b, b+1, b+2
+  uint32_t lb1 = BB, lb2 = 2 * BB, lb4 = 0;                   // B slots of stages x0+1, x0+2, x0+4
+  uint64_t a_nx = ra.a0 + 2 * kBK * 2;                        // A block b+2
+  uint64_t b_nx = ra.b0 + 4 * ra.b_step;                      // B stage x0+4
+  int xb = 4;                                                 // x0+4
+  bool mnow = mask_b == 0;                                    // block b applies the K mask
+  SlotDma da = a_dma(a_nx, 2, nb > 2 ? (uint32_t)kOobOffset : 0u), db0, db1;
+
+  uint32_t lim0, lim1;
+  uint64_t b_nx1;
   for (int b = 0; b < nb; ++b) {
-    const int x0 = 2 * b;
-    if (b == mask_b) mask_a_lanes<BM, BN>(L, wave, lane, kin_last);
-    {
-      // a block past K is loaded with an empty range: all lanes read zeros
-      // and nothing is fetched, so the loop needs no branches
-      const SlotDma da = a_dma(a_addr, sa2, b + 2 < nb ? (uint32_t)kOobOffset : 0u);
-      ring_step<BM, BN, 1>(acc, f0, f1, a_slot(sa0) + o.a_rd[1], b_slot(x0 + 1), o, da, da, L);
-    }
+    ring_step<BM, BN, 1>(acc, f0, f1, ra.lds0 + la0 + o.a_rd[1], lb1, o, da, da, L, [&]<int g>() {
+      if constexpr (g < R::APB) {
+        if (mnow && mk[g]) L.a_voff[g] = kOobOffset;
+      }
+      if constexpr (g == P1::stage_group(0, 6)) lim0 = b_stage_limit(ra, xb);
+      if constexpr (g == P1::stage_group(1, 6)) db0.rsrc = make_rsrc_addr(b_nx, lim0);
+      if constexpr (g == P1::stage_group(2, 6)) {
+        db0.m0 = b_m0w + lb4;
+        db1.m0 = b_m0w + lb1;
+      }
+      if constexpr (g == P1::stage_group(3, 6)) lim1 = b_stage_limit(ra, xb + 1);
+      if constexpr (g == P1::stage_group(4, 6)) b_nx1 = b_nx + ra.b_step;
+      if constexpr (g == P1::stage_group(5, 6)) db1.rsrc = make_rsrc_addr(b_nx1, lim1);
+    });
     wait_vmem_at_most<R::APB>();
     wait_lds_all();
     __syncthreads();
-    ring_step<BM, BN, 2>(acc, f1, f0, a_slot(sa1) + o.a_rd[0], b_slot(x0 + 2), o, b_dma(b_addr, x0 + 4),
-                         b_dma(b_addr + ra.b_step, x0 + 5), L);
-    sa0 = sa1;
-    sa1 = sa2;
-    sa2 = next3(sa2);
-    a_addr += kBK * 2;
-    b_addr += 2 * ra.b_step;
+    ring_step<BM, BN, 2>(acc, f1, f0, ra.lds0 + la1 + o.a_rd[0], lb2, o, db0, db1, L, [&]<int g>() {
+      if constexpr (g == P2::stage_group(0, 5)) {
+        const uint32_t t = la0;
+        la0 = la1;
+        la1 = la2;
+        la2 = t;
+      }
+      if constexpr (g == P2::stage_group(1, 5)) {
+        lb1 ^= 2 * BB;
+        lb2 ^= 2 * BB;
+        lb4 ^= 2 * BB;
+      }
+      if constexpr (g == P2::stage_group(2, 5)) a_nx += kBK * 2;
+      if constexpr (g == P2::stage_group(3, 5)) {
+        da.rsrc = make_rsrc_addr(a_nx, b + 3 < nb ? (uint32_t)kOobOffset : 0u);
+        da.m0 = a_m0w + la2;
+      }
+      if constexpr (g == P2::stage_group(4, 5)) {
+        b_nx += 2 * ra.b_step;
+        xb += 2;
+        mnow = b + 1 == mask_b;
+      }
+    });
   }
   // the last blocks' empty-range loads still write zeros into the ring: let
   // them land before the next task's prologue loads into the same slots
