@@ -128,6 +128,7 @@ __device__ __forceinline__ void wait_vmem_at_most() {
 }
 __device__ __forceinline__ void wait_lds_all() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 
+
 // ---- MFMA 16x16x32 fragments -------------------------------------------------------------
 // The MFMA takes the B fragment as its first operand, so it computes the
 // transposed 16x16 block: lane l ends with row l%16 of the fragment and its 4
@@ -387,11 +388,15 @@ struct StepPlan {
   static constexpr int NP1 = OP == 1 ? 0 : Ring<BM, BN>::BPW / 2;                      // pairs from d1
   static constexpr int NP = NP0 + NP1;
   static constexpr int ND = 3 * NP;
-  static constexpr int read_group(int r) { return (r * G) / NR; }
+  // the B step opens with G0 groups of MFMAs alone and then waits at the
+  // block's barrier: those MFMAs need nothing the barrier publishes, and they
+  // keep the matrix core busy while the waves meet
+  static constexpr int G0 = OP == 2 ? 2 : 0;
+  static constexpr int read_group(int r) { return G0 + (r * (G - G0)) / NR; }
   static constexpr int dma_group(int o) {
-    int g = -1;
+    int g = G0 - 1;
     for (int i = 0; i <= o; ++i) {
-      const int start = ((2 * (i / 3) + 1) * G) / (2 * NP) - 1 + i % 3;
+      const int start = G0 + ((2 * (i / 3) + 1) * (G - G0)) / (2 * NP) - 1 + i % 3;
       g = g + 1 > start ? g + 1 : start;
     }
     return g;
@@ -421,7 +426,7 @@ struct StepPlan {
     }
     return (s * G) / ns;
   }
-  static_assert(NR <= G, "one read per group");
+  static_assert(NR <= G - G0, "one read per group");
   static_assert(ND == 0 || dma_group(ND - 1) < G, "loads fit in the step");
 };
 
@@ -496,6 +501,16 @@ __device__ __forceinline__ void ring_group(Acc<BM, BN>& acc, const Frags<BM, BN>
   using P = StepPlan<BM, BN, OP>;
   constexpr int i = g / T::FN, j = g % T::FN;
   acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(cur.b[j], cur.a[i], acc[i][j], 0, 0, 0);
+  if constexpr (OP == 2 && g == P::G0) {
+    // the block's barrier: A block b+1 and B stages x0+2, x0+3 have landed for
+    // every wave (only the A block loaded in the A step may be in flight), and
+    // every wave's reads issued in the A step are done (among them the last
+    // reads of the B slot this step loads into, and of the A slot the next A
+    // step loads into)
+    wait_vmem_at_most<Ring<BM, BN>::APB>();
+    wait_lds_all();
+    __syncthreads();
+  }
   group_reads<BM, BN, OP, g>(a_base, b_slot, b_rd, br, nxt, std::make_integer_sequence<int, P::NR>{});
   group_dma<BM, BN, OP, g>(d0, d1, L, std::make_integer_sequence<int, P::ND>{});
   ex.template operator()<g>();
@@ -548,13 +563,14 @@ __device__ __forceinline__ uint32_t b_stage_limit(const RingAddr& ra, int x) {
 // stages x0 = 2b, x0+1, one 32-deep MFMA step each.  Each step runs the MFMAs
 // of one stage while it reads the operands of the next:
 //   step 1 (MFMAs of x0, reads A b/1 and B x0+1):  loads: A block b+2
-//   wait until A block b+1 and B stages x0+2, x0+3 have landed (A block b+2
-//   may still be in flight), barrier b
 //   step 2 (MFMAs of x0+1, reads A b+1/0 and B x0+2): loads: B stages x0+4, x0+5
+//     after its first MFMAs: wait until A block b+1 and B stages x0+2, x0+3
+//     have landed (A block b+2 may still be in flight) and this wave's reads
+//     are done, barrier b; then the reads and loads of step 2
 // A block kb lives in A slot kb mod 3, B stage x in B slot x mod 4.  Every load
-// goes into a slot whose last reads were issued before the barrier that
-// precedes the load; the shortest lead from a load to the barrier that
-// publishes it is one step.  The last blocks still issue their loads, for
+// goes into a slot whose last reads were done before the barrier that precedes
+// the load; the shortest lead from a load to the barrier that publishes it is
+// one step.  The last blocks still issue their loads, for
 // blocks and stages past K, with empty ranges (no memory is read, zeros land
 // in slots that are not read again), so that the loop has no branches.
 //
@@ -659,9 +675,6 @@ __device__ __forceinline__ void main_loop_ring(const RingAddr& ra, int nb, int64
       if constexpr (g == P1::stage_group(4, 6)) b_nx1 = b_nx + ra.b_step;
       if constexpr (g == P1::stage_group(5, 6)) db1.rsrc = make_rsrc_addr(b_nx1, lim1);
     });
-    wait_vmem_at_most<R::APB>();
-    wait_lds_all();
-    __syncthreads();
     ring_step<BM, BN, 2>(acc, f1, f0, ra.lds0 + la1 + o.a_rd[0], lb2, o, db0, db1, L, [&]<int g>() {
       if constexpr (g == P2::stage_group(0, 5)) {
         const uint32_t t = la0;
