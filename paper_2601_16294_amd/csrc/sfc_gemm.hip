@@ -245,6 +245,14 @@ __device__ __forceinline__ void dma16_pair(i32x4 rsrc, uint32_t m0_value, int v0
                :: "s"(m0_value), "v"(v0), "v"(v1), "s"(rsrc), "n"(OFF), "n"(OFF + 1024) : "memory");
 }
 
+// Make a scalar opaque to the optimiser, so that an update stays where the code
+// puts it (induction-variable rewriting would otherwise move the per-block
+// address updates together to the end of the loop body).
+template <typename V>
+__device__ __forceinline__ void pin_scalar(V& v) {
+  asm volatile("" : "+s"(v));
+}
+
 __device__ __forceinline__ i32x4 make_rsrc_addr(uint64_t a, uint32_t num_records) {
   i32x4 r = {(int)(uint32_t)a, (int)((uint32_t)(a >> 32) & 0xFFFFu), (int)num_records, 0x00020000};
   r[0] = __builtin_amdgcn_readfirstlane(r[0]);
@@ -687,7 +695,10 @@ __device__ __forceinline__ void main_loop_ring(const RingAddr& ra, int nb, int64
         lb2 ^= 2 * BB;
         lb4 ^= 2 * BB;
       }
-      if constexpr (g == P2::stage_group(2, 5)) a_nx += kBK * 2;
+      if constexpr (g == P2::stage_group(2, 5)) {
+        a_nx += kBK * 2;
+        pin_scalar(a_nx);
+      }
       if constexpr (g == P2::stage_group(3, 5)) {
         da.rsrc = make_rsrc_addr(a_nx, b + 3 < nb ? (uint32_t)kOobOffset : 0u);
         da.m0 = a_m0w + la2;
@@ -695,6 +706,8 @@ __device__ __forceinline__ void main_loop_ring(const RingAddr& ra, int nb, int64
       if constexpr (g == P2::stage_group(4, 5)) {
         b_nx += 2 * ra.b_step;
         xb += 2;
+        pin_scalar(b_nx);
+        pin_scalar(xb);
         mnow = b + 1 == mask_b;
       }
     });
