@@ -144,8 +144,9 @@ int sfc_gemm_plan(int64_t M, int64_t N, int64_t K, int ca_layers, int tile, int6
 /*
  * sfc_probe_mfma -- measurement aid for the roofline (the counterpart of the
  * paper's compute micro-benchmark, Section III.B): register-only bf16 MFMA
- * 32x32x16 throughput of the current device, 256 workgroups x 4 waves, each
- * wave running `iterations` rounds of 16 independent MFMAs.
+ * 16x16x32 throughput (the GEMM kernel's instruction) of the current device,
+ * 256 workgroups x 4 waves, each wave running `iterations` rounds of 64
+ * independent MFMAs.
  *   random_operands  1: operands drawn at random (they change between MFMAs, as
  *                    in a GEMM); 0: constant operands.
  *   tflops, mhz      out: achieved TFLOP/s and the mean shader clock sampled

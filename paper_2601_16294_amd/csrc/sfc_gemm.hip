@@ -20,9 +20,11 @@
 //   * fast path (16-byte aligned rows): A and B go straight from global memory
 //     into LDS with buffer loads (lanes outside the matrix read zeros), A in a
 //     ring of three 64-deep block slots [BM][64], B in a ring of four 32-deep
-//     stage slots [32][BN], with one barrier per 64-deep block.  The loads of
-//     the blocks two ahead are spread one pair per few MFMAs over the steps,
-//     so the texture path never sees a burst;
+//     stage slots [32][BN], with one barrier per 64-deep block.  Every
+//     32-deep step has a fixed plan: one MFMA per group, beside it at most one
+//     fragment read of the next step and one load operation for the blocks
+//     ahead, and small pieces of the scalar bookkeeping (a wave issues one
+//     instruction every 4 cycles, a 16x16x32 MFMA takes 16);
 //   * general path (any alignment): elements assembled in registers, two
 //     64-deep LDS buffers;
 //   * the MFMA B operand is read from [k][n] with the transposing LDS read

@@ -301,7 +301,8 @@ int sfc_probe_mfma(int random_operands, int iterations, double* tflops, double* 
   double sum = 0.0;
   for (int i = 0; i < 256; ++i) sum += clk[i];
   *mhz = sum / 256.0;
-  const double flops = 256.0 * 4.0 * (double)iterations * 16.0 * (2.0 * 32 * 32 * 16);
+  // per wave and round: 64 MFMA 16x16x32
+  const double flops = 256.0 * 4.0 * (double)iterations * 64.0 * (2.0 * 16 * 16 * 32);
   *tflops = ms > 0.0 ? flops / (ms * 1e-3) / 1e12 : 0.0;
   return SFC_OK;
 }
