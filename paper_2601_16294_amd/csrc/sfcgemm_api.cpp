@@ -103,14 +103,16 @@ int tile_from_api(int t) {
 // Block shape for SFC_TILE_AUTO: the shape with the smallest estimated time.
 // A CU runs `occ` workgroups at once and completes a BM x BN block at a rate
 // proportional to rate[] (measured on MI355X with the 8192^3 bf16 GEMM, where
-// every shape fills whole rounds); the persistent grid takes ceil(tasks /
-// (CUs * occ)) rounds, each costing occ * BM * BN / rate.  Ties keep the
-// earlier shape.
+// the three larger shapes fill whole rounds; the 128x128 rate is taken from
+// shapes where it does not thrash L2); the persistent grid takes
+// ceil(tasks / (CUs * occ)) rounds, each costing occ * BM * BN / rate.  Near
+// ties go to the shape that computes fewer padded elements (ragged edges),
+// then to the earlier shape.
 int choose_tile(DeviceState& st, int64_t M, int64_t N, int ce, bool ob, bool vec, int* tile) {
   static const int order[4] = {sfc::kT256x256, sfc::kT128x256, sfc::kT256x128, sfc::kT128x128};
-  static const double rate[4] = {1.0, 0.93, 0.93, 0.67};
+  static const double rate[4] = {1.0, 0.85, 0.85, 0.75};
   int best = sfc::kT256x256;
-  double best_t = 1e300;
+  double best_t = 1e300, best_pad = 1e300;
   for (int i = 0; i < 4; ++i) {
     const int t = order[i];
     int occ = 1;
@@ -120,7 +122,12 @@ int choose_tile(DeviceState& st, int64_t M, int64_t N, int ce, bool ob, bool vec
     const int64_t tasks = sfc::ceil_div(M, bm) * sfc::ceil_div(N, bn) * ce;
     const int64_t rounds = sfc::ceil_div(tasks, (int64_t)st.num_cus * occ);
     const double est = (double)rounds * (double)occ * (double)(bm * bn) / rate[i];
-    if (est < best_t * 0.999) { best_t = est; best = t; }
+    const double pad = (double)tasks * (double)(bm * bn);
+    if (est < best_t * 0.999 || (est < best_t * 1.001 && pad < best_pad)) {
+      best_t = est;
+      best_pad = pad;
+      best = t;
+    }
   }
   *tile = best;
   return SFC_OK;
