@@ -221,20 +221,28 @@ __device__ __forceinline__ void mma_step(const Frags<BM, BN>& cur, Acc<BM, BN>& 
 // (LDS reads, loads, address arithmetic) to a few instructions per MFMA,
 // spread evenly.
 constexpr int kSK = 32;        // K depth of one B stage (one MFMA step)
-constexpr int kASlots = 3;     // A block slots
-constexpr int kBSlots = 4;     // B stage slots
 constexpr int kBias = 4096;    // bytes; keeps every biased voffset positive
 
+// The loads of block b+D are issued during block b (prefetch depth D): the A
+// ring has D+1 block slots, the B ring 2D stage slots.  D = 3 where the LDS
+// holds that at the same occupancy (128x256: exactly 160 KiB), else 2.
 template <int BM, int BN>
 struct Ring {
   static constexpr int A_BLK = BM * kBK;                 // elements of one A block
   static constexpr int B_STG = kSK * BN;                 // elements of one B stage
   static constexpr int A_BYTES = A_BLK * 2, B_BYTES = B_STG * 2;
-  static constexpr int B_OFF = kASlots * A_BYTES;        // byte offset of the B slots
+  static constexpr int D = (BM == 128 && BN == 256) ? 3 : 2;
+  static constexpr int NA = D + 1, NB = 2 * D;           // A block slots, B stage slots
+  static constexpr int B_OFF = NA * A_BYTES;             // byte offset of the B slots
   static constexpr int APB = A_BYTES / 1024 / 4;         // A loads per wave per block
   static constexpr int BPW = B_BYTES / 1024 / 4;         // B loads per wave per stage
-  static constexpr int ELEMS = kASlots * A_BLK + kBSlots * B_STG;
+  static constexpr int ELEMS = NA * A_BLK + NB * B_STG;
+  // loads younger than block b+1's, when block b's barrier waits for it
+  static constexpr int IN_FLIGHT = (D - 2) * (APB + 2 * BPW) + APB;
   static_assert(APB % 4 == 0 && (BPW == 2 || BPW == 4), "tile shape");
+  static_assert(ELEMS * 2 <= 160 * 1024, "LDS of one CU");
+  static_assert(IN_FLIGHT <= 63, "vmcnt range");
+  static_assert(D == 2 || D == 3, "ring depth");
 };
 
 // Two loads sharing M0: LDS M0+OFF+16*lane and M0+OFF+1024+16*lane.
@@ -517,7 +525,7 @@ __device__ __forceinline__ void ring_group(Acc<BM, BN>& acc, const Frags<BM, BN>
     // every wave's reads issued in the A step are done (among them the last
     // reads of the B slot this step loads into, and of the A slot the next A
     // step loads into)
-    wait_vmem_at_most<Ring<BM, BN>::APB>();
+    wait_vmem_at_most<Ring<BM, BN>::IN_FLIGHT>();
     wait_lds_all();
     __syncthreads();
   }
@@ -572,17 +580,18 @@ __device__ __forceinline__ uint32_t b_stage_limit(const RingAddr& ra, int x) {
 // The K loop of one task over nb 64-deep blocks.  Block b = A block b and B
 // stages x0 = 2b, x0+1, one 32-deep MFMA step each.  Each step runs the MFMAs
 // of one stage while it reads the operands of the next:
-//   step 1 (MFMAs of x0, reads A b/1 and B x0+1):  loads: A block b+2
-//   step 2 (MFMAs of x0+1, reads A b+1/0 and B x0+2): loads: B stages x0+4, x0+5
+//   step 1 (MFMAs of x0, reads A b/1 and B x0+1):  loads: A block b+D
+//   step 2 (MFMAs of x0+1, reads A b+1/0 and B x0+2): loads: B stages x0+2D, x0+2D+1
 //     after its first MFMAs: wait until A block b+1 and B stages x0+2, x0+3
-//     have landed (A block b+2 may still be in flight) and this wave's reads
-//     are done, barrier b; then the reads and loads of step 2
-// A block kb lives in A slot kb mod 3, B stage x in B slot x mod 4.  Every load
-// goes into a slot whose last reads were done before the barrier that precedes
-// the load; the shortest lead from a load to the barrier that publishes it is
-// one step.  The last blocks still issue their loads, for
-// blocks and stages past K, with empty ranges (no memory is read, zeros land
-// in slots that are not read again), so that the loop has no branches.
+//     have landed (the loads issued after them may still be in flight) and
+//     this wave's reads are done, barrier b; then the reads and loads of step 2
+// A block kb lives in A slot kb mod (D+1), B stage x in B slot x mod 2D.  Every
+// load goes into a slot whose last reads were done before the barrier that
+// precedes the load; the shortest lead from a load to the barrier that
+// publishes it is 2D-3 steps.  The prologue issues blocks 0 .. D-1; the last
+// blocks still issue their loads, for blocks and stages past K, with empty
+// ranges (no memory is read, zeros land in slots that are not read again), so
+// that the loop has no branches.
 //
 // The scalar bookkeeping (slot addresses, descriptors, limits) is carried from
 // block to block and updated in small pieces on chosen groups of the steps:
@@ -592,7 +601,7 @@ __device__ __forceinline__ uint32_t b_stage_limit(const RingAddr& ra, int x) {
 // When the last block runs past K (kin_last < 64): B rows at or past K fall
 // outside the B descriptors' ranges and read zeros; A block nb-1 is loaded with
 // its lanes past K masked (selects on the first groups of the step that issues
-// those loads, the last A loads of the task).
+// those loads, or in the prologue when nb <= D).
 template <int BM, int BN>
 __device__ __forceinline__ void main_loop_ring(const RingAddr& ra, int nb, int64_t kin_last,
                                                const ReadOffsets<BM, BN>& o, RingLanes<BM, BN>& L, int lane,
@@ -601,8 +610,8 @@ __device__ __forceinline__ void main_loop_ring(const RingAddr& ra, int nb, int64
   using T = Tile<BM, BN>;
   using P1 = StepPlan<BM, BN, 1>;
   using P2 = StepPlan<BM, BN, 2>;
+  constexpr int D = R::D;
   constexpr uint32_t BB = (uint32_t)R::B_BYTES;
-  static_assert((BB & (BB - 1)) == 0, "B slot size is a power of two");
   const int wave = ra.wave;
   const bool masked = kin_last < kBK;
   const uint32_t a_m0w = ra.lds0 + (uint32_t)(wave * R::APB * 1024);            // this wave's segment, A slot 0
@@ -613,26 +622,39 @@ __device__ __forceinline__ void main_loop_ring(const RingAddr& ra, int nb, int64
     d.m0 = a_m0w + (uint32_t)(slot * R::A_BYTES);
     return d;
   };
-  auto b_dma = [&](uint64_t addr, int x) {
+  auto b_dma = [&](uint64_t addr, int x, int slot) {
     SlotDma d;
     d.rsrc = make_rsrc_addr(addr, b_stage_limit(ra, x));
-    d.m0 = b_m0w + (uint32_t)((x & (kBSlots - 1)) * R::B_BYTES);
+    d.m0 = b_m0w + (uint32_t)(slot * R::B_BYTES);
     return d;
   };
 
-  // prologue: A block 0 and B stages 0, 1, then A block 1 and B stages 2, 3
-  if (masked && nb == 1) mask_a_lanes<BM, BN>(L, wave, lane, kin_last);
-  dma_all<BM, BN, 1>(a_dma(ra.a0, 0, kOobOffset), L);
-  dma_all<BM, BN, 2>(b_dma(ra.b0, 0), L);
-  dma_all<BM, BN, 2>(b_dma(ra.b0 + ra.b_step, 1), L);
-  if (nb > 1) {
-    if (masked && nb == 2) mask_a_lanes<BM, BN>(L, wave, lane, kin_last);
-    dma_all<BM, BN, 1>(a_dma(ra.a0 + kBK * 2, 1, kOobOffset), L);
-    dma_all<BM, BN, 2>(b_dma(ra.b0 + 2 * ra.b_step, 2), L);
-    dma_all<BM, BN, 2>(b_dma(ra.b0 + 3 * ra.b_step, 3), L);
-    wait_vmem_at_most<R::APB + 2 * R::BPW>();
+  // prologue: blocks 0 .. D-1 (A block k into A slot k, B stages 2k, 2k+1 into
+  // B slots 2k, 2k+1), then wait for block 0.  Depth 2 loads block 1 only when
+  // there is one; deeper rings load blocks past K with empty ranges.
+  if constexpr (D == 2) {
+    if (masked && nb == 1) mask_a_lanes<BM, BN>(L, wave, lane, kin_last);
+    dma_all<BM, BN, 1>(a_dma(ra.a0, 0, kOobOffset), L);
+    dma_all<BM, BN, 2>(b_dma(ra.b0, 0, 0), L);
+    dma_all<BM, BN, 2>(b_dma(ra.b0 + ra.b_step, 1, 1), L);
+    if (nb > 1) {
+      if (masked && nb == 2) mask_a_lanes<BM, BN>(L, wave, lane, kin_last);
+      dma_all<BM, BN, 1>(a_dma(ra.a0 + kBK * 2, 1, kOobOffset), L);
+      dma_all<BM, BN, 2>(b_dma(ra.b0 + 2 * ra.b_step, 2, 2), L);
+      dma_all<BM, BN, 2>(b_dma(ra.b0 + 3 * ra.b_step, 3, 3), L);
+      wait_vmem_at_most<R::APB + 2 * R::BPW>();
+    } else {
+      wait_vmem_at_most<0>();
+    }
   } else {
-    wait_vmem_at_most<0>();
+#pragma unroll
+    for (int k = 0; k < D; ++k) {
+      if (masked) mask_a_lanes_if<BM, BN>(L, wave, lane, kin_last, k == nb - 1);
+      dma_all<BM, BN, 1>(a_dma(ra.a0 + (uint64_t)k * (kBK * 2), k, k < nb ? (uint32_t)kOobOffset : 0u), L);
+      dma_all<BM, BN, 2>(b_dma(ra.b0 + (uint64_t)(2 * k) * ra.b_step, 2 * k, 2 * k), L);
+      dma_all<BM, BN, 2>(b_dma(ra.b0 + (uint64_t)(2 * k + 1) * ra.b_step, 2 * k + 1, 2 * k + 1), L);
+    }
+    wait_vmem_at_most<(D - 1) * (R::APB + 2 * R::BPW)>();
   }
   __syncthreads();
 
@@ -652,21 +674,22 @@ __device__ __forceinline__ void main_loop_ring(const RingAddr& ra, int nb, int64
     }
   }
 
-  // per-lane K-mask condition of each A load (used on block nb-3, whose step 1
-  // loads A block nb-1; from nb <= 2 on the prologue has masked)
+  // per-lane K-mask condition of each A load (used on block nb-1-D, whose A
+  // step loads A block nb-1; for nb <= D the prologue has masked)
   bool mk[R::APB];
 #pragma unroll
   for (int j = 0; j < R::APB; ++j) mk[j] = a_load_k(wave, R::APB, j, lane) >= kin_last;
-  const int mask_b = masked ? nb - 3 : -1;
+  const int mask_b = masked ? nb - 1 - D : -1;
 
   // scalar state of block b
-  uint32_t la0 = 0, la1 = R::A_BYTES, la2 = 2 * R::A_BYTES;   // A slots of blocks b, b+1, b+2
-  uint32_t lb1 = BB, lb2 = 2 * BB, lb4 = 0;                   // B slots of stages x0+1, x0+2, x0+4
-  uint64_t a_nx = ra.a0 + 2 * kBK * 2;                        // A block b+2
-  uint64_t b_nx = ra.b0 + 4 * ra.b_step;                      // B stage x0+4
-  int xb = 4;                                                 // x0+4
-  bool mnow = mask_b == 0;                                    // block b applies the K mask
-  SlotDma da = a_dma(a_nx, 2, nb > 2 ? (uint32_t)kOobOffset : 0u), db0, db1;
+  // A slots of blocks b, b+1, b+2 (and b+3 for depth 3)
+  uint32_t la0 = 0, la1 = R::A_BYTES, la2 = 2 * R::A_BYTES, la3 = 3 * R::A_BYTES;
+  uint32_t sb = 0, lb1 = BB, lb2 = 2 * BB;  // B slots of stages x0 (and x0+2D), x0+1 (and x0+2D+1), x0+2
+  uint64_t a_nx = ra.a0 + D * kBK * 2;      // A block b+D
+  uint64_t b_nx = ra.b0 + 2 * D * ra.b_step; // B stage x0+2D
+  int xb = 2 * D;                           // x0+2D
+  bool mnow = mask_b == 0;                  // block b applies the K mask
+  SlotDma da = a_dma(a_nx, D, D < nb ? (uint32_t)kOobOffset : 0u), db0, db1;
 
   uint32_t lim0, lim1;
   uint64_t b_nx1;
@@ -678,7 +701,7 @@ __device__ __forceinline__ void main_loop_ring(const RingAddr& ra, int nb, int64
       if constexpr (g == P1::stage_group(0, 6)) lim0 = b_stage_limit(ra, xb);
       if constexpr (g == P1::stage_group(1, 6)) db0.rsrc = make_rsrc_addr(b_nx, lim0);
       if constexpr (g == P1::stage_group(2, 6)) {
-        db0.m0 = b_m0w + lb4;
+        db0.m0 = b_m0w + sb;
         db1.m0 = b_m0w + lb1;
       }
       if constexpr (g == P1::stage_group(3, 6)) lim1 = b_stage_limit(ra, xb + 1);
@@ -690,20 +713,31 @@ __device__ __forceinline__ void main_loop_ring(const RingAddr& ra, int nb, int64
         const uint32_t t = la0;
         la0 = la1;
         la1 = la2;
-        la2 = t;
+        if constexpr (D == 2) {
+          la2 = t;
+        } else {
+          la2 = la3;
+          la3 = t;
+        }
       }
       if constexpr (g == P2::stage_group(1, 5)) {
-        lb1 ^= 2 * BB;
-        lb2 ^= 2 * BB;
-        lb4 ^= 2 * BB;
+        if constexpr (R::NB == 4) {
+          sb ^= 2 * BB;
+          lb1 ^= 2 * BB;
+          lb2 ^= 2 * BB;
+        } else {
+          sb = lb2;
+          lb1 = lb2 + BB;
+          lb2 = lb2 + 2 * BB == (uint32_t)R::NB * BB ? 0u : lb2 + 2 * BB;
+        }
       }
       if constexpr (g == P2::stage_group(2, 5)) {
         a_nx += kBK * 2;
         pin_scalar(a_nx);
       }
       if constexpr (g == P2::stage_group(3, 5)) {
-        da.rsrc = make_rsrc_addr(a_nx, b + 3 < nb ? (uint32_t)kOobOffset : 0u);
-        da.m0 = a_m0w + la2;
+        da.rsrc = make_rsrc_addr(a_nx, b + 1 + D < nb ? (uint32_t)kOobOffset : 0u);
+        da.m0 = a_m0w + (D == 2 ? la2 : la3);
       }
       if constexpr (g == P2::stage_group(4, 5)) {
         b_nx += 2 * ra.b_step;
