@@ -181,8 +181,14 @@ def main():
         whm_num = whm_den = 0.0
         for name, wl in W.items():
             entry = {"flops": wl.flops, "tile": wl.tile, "gemms": [list((x.M, x.N, x.K)) for x in wl.gemms]}
+            # what the library's analytical model picks for each GEMM (SFC_CA_AUTO)
+            entry["model_choice"] = []
+            for x in wl.gemms:
+                pm = sg.sfc_gemm_plan(x.M, x.N, x.K, 0, wl.tile)
+                entry["model_choice"].append({"tile": f"{pm['BM']}x{pm['BN']}", "ca_layers": pm["layers"]})
             per_c = {}
             for c in wl.ca_layers:
+                label = "auto" if c == 0 else c
                 cold_t = warm_t = 0.0
                 for gg in wl.gemms:
                     _, _, a, b, cc = prepare(gg)
@@ -206,10 +212,10 @@ def main():
                     torch.cuda.synchronize()
                     warm_t += s.elapsed_time(e) / args.reps
                     del a, b, cc
-                per_c[c] = {"cold_ms": round(cold_t, 4), "warm_ms": round(warm_t, 4),
-                            "tflops_cold": round(wl.flops / (cold_t * 1e-3) / 1e12, 2),
-                            "tflops_warm": round(wl.flops / (warm_t * 1e-3) / 1e12, 2)}
-                log(f"[bench] {name} c={c}: {per_c[c]}")
+                per_c[label] = {"cold_ms": round(cold_t, 4), "warm_ms": round(warm_t, 4),
+                                "tflops_cold": round(wl.flops / (cold_t * 1e-3) / 1e12, 2),
+                                "tflops_warm": round(wl.flops / (warm_t * 1e-3) / 1e12, 2)}
+                log(f"[bench] {name} c={label}: {per_c[label]}")
             best_c = max(per_c, key=lambda k: per_c[k]["tflops_cold"])
             best = per_c[best_c]
             entry.update({"per_ca_layers": per_c if len(per_c) > 1 else None, "best_ca_layers": best_c,

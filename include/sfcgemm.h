@@ -54,6 +54,11 @@ extern "C" {
 #define SFC_TILE_128x256 3       /* BM = 128, BN = 256 */
 #define SFC_TILE_256x256 4
 
+/* ---- number of K layers (copies of C) ---------------------------------- */
+#define SFC_CA_AUTO      0       /* ca_layers = 0: chosen with the block shape by the
+                                    analytical model (Section III.B Eq. 1-4, used as in
+                                    Section III.C's second option), among 1, 2, 4, 8 */
+
 /* ---- order of the output blocks ---------------------------------------- */
 #define SFC_ORDER_HILBERT   0    /* generalized Hilbert curve (Section II.B) */
 #define SFC_ORDER_ROW_MAJOR 1    /* plain row-major; for comparison only */
@@ -94,6 +99,7 @@ int sfc_tile_order_ex(int gm, int gn, int order, int32_t *out_idx);
  *              sfc_gemm_ws_size() bytes that the library allocates once per
  *              device and reuses; concurrent c > 1 calls on different streams
  *              must use sfc_gemm_ex with their own workspaces.
+ *              SFC_CA_AUTO (0): the model picks c (see sfc_gemm_model).
  *   stream     hipStream_t or NULL.
  */
 int sfc_gemm(int64_t M, int64_t N, int64_t K,
@@ -112,7 +118,8 @@ int sfc_gemm_bf16out(int64_t M, int64_t N, int64_t K,
 /*
  * sfc_gemm_ws_size -- bytes of fp32 workspace that a ca_layers = c call needs:
  * c_eff * M * N * 4 with c_eff = min(c, ceil(K/64)) when c_eff > 1, else 0.
- * Returns 0 for invalid arguments as well.
+ * For c = SFC_CA_AUTO: the size for the largest count the model picks (8), a
+ * bound that holds whatever it chooses.  Returns 0 for invalid arguments as well.
  */
 size_t sfc_gemm_ws_size(int64_t M, int64_t N, int64_t K, int ca_layers);
 
@@ -134,12 +141,39 @@ int sfc_gemm_ex(int64_t M, int64_t N, int64_t K,
                 void *ws, size_t ws_bytes, void *stream);
 
 /*
- * sfc_gemm_plan -- what sfc_gemm_ex would launch, without launching.
+ * sfc_gemm_plan -- what sfc_gemm_ex would launch, without launching
+ * (fp32 output, 16-byte aligned operands).  ca_layers may be SFC_CA_AUTO and
+ * tile SFC_TILE_AUTO; the plan then shows the model's choice.
  *   plan[0] = BM, plan[1] = BN, plan[2] = gm, plan[3] = gn, plan[4] = c_eff,
  *   plan[5] = number of persistent workgroups, plan[6] = workgroups per CU.
  * Needs a device (it queries the CU count and kernel occupancy).
  */
 int sfc_gemm_plan(int64_t M, int64_t N, int64_t K, int ca_layers, int tile, int64_t plan[7]);
+
+/*
+ * sfc_gemm_model -- the analytical model behind SFC_TILE_AUTO and SFC_CA_AUTO,
+ * evaluated for given device parameters (host only: no device is touched).
+ * The paper's fine-grained roofline (Section III.B, Eq. 1-4) on the GPU: a core
+ * is a CU running `occupancy` persistent workgroups, one BRGEMM is one 64-deep
+ * block of one task, at max(G*gamma, beta*(S_A + S_B)) with the panels of a
+ * block shared by the tasks in flight on one XCD; the critical path is the
+ * rounds of tasks times the blocks of the longest layer, plus the C traffic
+ * (and, with layers, the copies written and read back) and the launches.
+ * Every candidate (block shape x c in {1, 2, 4, 8}, or only the fixed ones) is
+ * evaluated and the fastest kept; near ties go to less padded work, then to
+ * 256x256, 128x256, 256x128, 128x128 in that order, then to fewer layers.
+ *   out_type   SFC_OUT_F32 or SFC_OUT_BF16 (bytes of C).
+ *   ca_layers  SFC_CA_AUTO (0) or a fixed count in [1, 64].
+ *   tile       SFC_TILE_AUTO or a fixed SFC_TILE_*.
+ *   num_cus    compute units (>= 1).
+ *   occupancy  host array: workgroups per CU of SFC_TILE_128x128, _256x128,
+ *              _128x256, _256x256 (each >= 1).
+ *   choice     host out: [0] SFC_TILE_* code, [1] effective layer count,
+ *              [2] estimated shader clocks.
+ * Returns SFC_OK or SFC_ERR_INVALID_ARG.
+ */
+int sfc_gemm_model(int64_t M, int64_t N, int64_t K, int out_type, int ca_layers, int tile, int num_cus,
+                   const int32_t occupancy[4], int64_t choice[3]);
 
 /*
  * sfc_probe_mfma -- measurement aid for the roofline (the counterpart of the

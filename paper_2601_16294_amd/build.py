@@ -19,7 +19,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libsfcgemm.so")
-SOURCES = ["sfc_order.hip", "sfc_gemm.hip", "sfc_reduce.hip", "sfc_probe.hip", "sfcgemm_api.cpp"]
+SOURCES = ["sfc_order.hip", "sfc_gemm.hip", "sfc_reduce.hip", "sfc_probe.hip", "sfc_model.cpp",
+           "sfcgemm_api.cpp"]
 ARCH = "gfx950"
 
 

@@ -10,6 +10,7 @@
 namespace sfc {
 
 constexpr int kMaxLayers = 64;
+constexpr int kAutoLayers = 8;                  // largest layer count SFC_CA_AUTO picks
 constexpr int64_t kMaxDim = (int64_t)1 << 31;   // block indices are int32
 
 struct Checked {
@@ -50,8 +51,8 @@ inline Checked check_gemm_args(int64_t M, int64_t N, int64_t K, const void* A, i
   if (M < 0 || N < 0 || K < 0) return fail(SFC_ERR_INVALID_ARG, "M, N, K must be >= 0");
   if (out_type != SFC_OUT_F32 && out_type != SFC_OUT_BF16)
     return fail(SFC_ERR_INVALID_ARG, "unknown out_type");
-  if (ca_layers < 1 || ca_layers > kMaxLayers)
-    return fail(SFC_ERR_INVALID_ARG, "ca_layers must be in [1, 64]");
+  if (ca_layers < 0 || ca_layers > kMaxLayers)
+    return fail(SFC_ERR_INVALID_ARG, "ca_layers must be 0 (chosen by the model) or in [1, 64]");
   if (tile < SFC_TILE_AUTO || tile > SFC_TILE_256x256) return fail(SFC_ERR_INVALID_ARG, "unknown tile");
   if (order != SFC_ORDER_HILBERT && order != SFC_ORDER_ROW_MAJOR)
     return fail(SFC_ERR_INVALID_ARG, "unknown order");
@@ -75,7 +76,8 @@ inline Checked check_gemm_args(int64_t M, int64_t N, int64_t K, const void* A, i
   // the smallest block is 128 x 128
   if (ceil_div(M, 128) * ceil_div(N, 128) >= kMaxDim)
     return fail(SFC_ERR_UNSUPPORTED, "too many output blocks");
-  const int ce = effective_layers(K, ca_layers, 64);
+  // the model chooses at most kAutoLayers layers: check the largest case
+  const int ce = effective_layers(K, ca_layers == 0 ? kAutoLayers : ca_layers, 64);
   // task indices (blocks x layers) are 32-bit in the kernel
   if (ceil_div(M, 128) * ceil_div(N, 128) * ce >= kMaxDim)
     return fail(SFC_ERR_UNSUPPORTED, "too many output blocks x layers");
@@ -88,8 +90,8 @@ inline Checked check_gemm_args(int64_t M, int64_t N, int64_t K, const void* A, i
 }
 
 inline size_t ws_size(int64_t M, int64_t N, int64_t K, int ca_layers) {
-  if (M < 0 || N < 0 || K < 0 || ca_layers < 1 || ca_layers > kMaxLayers) return 0;
-  const int ce = effective_layers(K, ca_layers, 64);
+  if (M < 0 || N < 0 || K < 0 || ca_layers < 0 || ca_layers > kMaxLayers) return 0;
+  const int ce = effective_layers(K, ca_layers == 0 ? kAutoLayers : ca_layers, 64);
   if (ce <= 1) return 0;
   return (size_t)ce * (size_t)M * (size_t)N * 4u;
 }

@@ -11,6 +11,7 @@
 #include <string>
 #include <tuple>
 
+#include "sfc_model.h"
 #include "sfc_params.h"
 #include "sfc_validate.h"
 #include "sfcgemm.h"
@@ -100,39 +101,6 @@ int tile_from_api(int t) {
   }
 }
 
-// Block shape for SFC_TILE_AUTO: the shape with the smallest estimated time.
-// A CU runs `occ` workgroups at once and completes a BM x BN block at a rate
-// proportional to rate[] (measured on MI355X with the 8192^3 bf16 GEMM, where
-// the three larger shapes fill whole rounds; the 128x128 rate is taken from
-// shapes where it does not thrash L2); the persistent grid takes
-// ceil(tasks / (CUs * occ)) rounds, each costing occ * BM * BN / rate.  Near
-// ties go to the shape that computes fewer padded elements (ragged edges),
-// then to the earlier shape.
-int choose_tile(DeviceState& st, int64_t M, int64_t N, int ce, bool ob, bool vec, int* tile) {
-  static const int order[4] = {sfc::kT256x256, sfc::kT128x256, sfc::kT256x128, sfc::kT128x128};
-  static const double rate[4] = {1.0, 0.85, 0.85, 0.75};
-  int best = sfc::kT256x256;
-  double best_t = 1e300, best_pad = 1e300;
-  for (int i = 0; i < 4; ++i) {
-    const int t = order[i];
-    int occ = 1;
-    const int rc = get_occupancy(st, t, ob && ce == 1, vec, &occ);
-    if (rc != SFC_OK) return rc;
-    const int64_t bm = sfc::tile_bm(t), bn = sfc::tile_bn(t);
-    const int64_t tasks = sfc::ceil_div(M, bm) * sfc::ceil_div(N, bn) * ce;
-    const int64_t rounds = sfc::ceil_div(tasks, (int64_t)st.num_cus * occ);
-    const double est = (double)rounds * (double)occ * (double)(bm * bn) / rate[i];
-    const double pad = (double)tasks * (double)(bm * bn);
-    if (est < best_t * 0.999 || (est < best_t * 1.001 && pad < best_pad)) {
-      best_t = est;
-      best_pad = pad;
-      best = t;
-    }
-  }
-  *tile = best;
-  return SFC_OK;
-}
-
 struct Plan {
   int tile, bm, bn, gm, gn, ce, nk, grid, occ;
   bool vec;
@@ -140,15 +108,24 @@ struct Plan {
 
 int make_plan(DeviceState& st, int64_t M, int64_t N, int64_t K, const void* A, int64_t lda,
               const void* B, int64_t ldb, bool ob, int ca_layers, int tile_api, Plan* pl) {
-  pl->ce = sfc::effective_layers(K, ca_layers, sfc::kBK);
   // the fast path needs at least one K block per task
   pl->vec = K > 0 && sfc::vector_loads_ok(A, lda, B, ldb, K, N);
   int rc = SFC_OK;
-  if (tile_api == SFC_TILE_AUTO) {
-    rc = choose_tile(st, M, N, pl->ce, ob, pl->vec, &pl->tile);
-    if (rc != SFC_OK) return rc;
+  if (tile_api == SFC_TILE_AUTO || ca_layers == SFC_CA_AUTO) {
+    // the analytical model evaluates the free knobs (block shape, layers)
+    int occ[sfc::kNumTiles];
+    for (int t = 0; t < sfc::kNumTiles; ++t) {
+      rc = get_occupancy(st, t, ob && ca_layers == 1, pl->vec, &occ[t]);
+      if (rc != SFC_OK) return rc;
+    }
+    const sfc::ModelChoice ch =
+        sfc::model_choose(M, N, K, ob ? 2 : 4, st.num_cus, occ,
+                          tile_api == SFC_TILE_AUTO ? -1 : tile_from_api(tile_api), ca_layers);
+    pl->tile = ch.tile;
+    pl->ce = sfc::effective_layers(K, ch.layers, sfc::kBK);
   } else {
     pl->tile = tile_from_api(tile_api);
+    pl->ce = sfc::effective_layers(K, ca_layers, sfc::kBK);
   }
   pl->bm = sfc::tile_bm(pl->tile);
   pl->bn = sfc::tile_bn(pl->tile);
@@ -316,7 +293,7 @@ int sfc_probe_mfma(int random_operands, int iterations, double* tflops, double* 
 
 int sfc_gemm_plan(int64_t M, int64_t N, int64_t K, int ca_layers, int tile, int64_t plan[7]) {
   if (!plan) return set_error(SFC_ERR_INVALID_ARG, "plan is NULL");
-  if (M <= 0 || N <= 0 || K < 0 || ca_layers < 1 || ca_layers > sfc::kMaxLayers ||
+  if (M <= 0 || N <= 0 || K < 0 || ca_layers < 0 || ca_layers > sfc::kMaxLayers ||
       tile < SFC_TILE_AUTO || tile > SFC_TILE_256x256)
     return set_error(SFC_ERR_INVALID_ARG, "invalid plan arguments");
   std::lock_guard<std::mutex> lock(g_mu);
@@ -330,6 +307,25 @@ int sfc_gemm_plan(int64_t M, int64_t N, int64_t K, int ca_layers, int tile, int6
   if (rc != SFC_OK) return rc;
   plan[0] = pl.bm; plan[1] = pl.bn; plan[2] = pl.gm; plan[3] = pl.gn;
   plan[4] = pl.ce; plan[5] = pl.grid; plan[6] = pl.occ;
+  return SFC_OK;
+}
+
+int sfc_gemm_model(int64_t M, int64_t N, int64_t K, int out_type, int ca_layers, int tile, int num_cus,
+                   const int32_t occupancy[4], int64_t choice[3]) {
+  if (!choice || !occupancy) return set_error(SFC_ERR_INVALID_ARG, "NULL model argument");
+  if (M < 0 || N < 0 || K < 0 || num_cus < 1 || ca_layers < 0 || ca_layers > sfc::kMaxLayers ||
+      tile < SFC_TILE_AUTO || tile > SFC_TILE_256x256 || (out_type != SFC_OUT_F32 && out_type != SFC_OUT_BF16))
+    return set_error(SFC_ERR_INVALID_ARG, "invalid model arguments");
+  int occ[sfc::kNumTiles];
+  for (int t = 0; t < sfc::kNumTiles; ++t) {
+    if (occupancy[t] < 1) return set_error(SFC_ERR_INVALID_ARG, "occupancy must be >= 1");
+    occ[t] = occupancy[t];
+  }
+  const sfc::ModelChoice ch = sfc::model_choose(M, N, K, out_type == SFC_OUT_BF16 ? 2 : 4, num_cus, occ,
+                                                tile == SFC_TILE_AUTO ? -1 : tile_from_api(tile), ca_layers);
+  choice[0] = ch.tile + 1;   // SFC_TILE_* code
+  choice[1] = sfc::effective_layers(K, ch.layers, sfc::kBK);
+  choice[2] = (int64_t)(ch.clk + 0.5);
   return SFC_OK;
 }
 

@@ -99,7 +99,7 @@ def workloads() -> List[Workload]:
         Workload("ragged3000x7000x2048_f32out", [Gemm(3000, 7000, 2048, U, U, 3001, 3002)]),
         Workload("kdominant1024x1024x65536_f32out",
                  [Gemm(1024, 1024, 65536, ("normal", 0.0, 0.1), ("normal", 0.0, 0.1), 4001, 4002)],
-                 ca_layers=[1, 2, 4, 8]),
+                 ca_layers=[1, 2, 4, 8, 0]),     # 0: the count the library's model picks
         Workload("prefill4096_bf16out",
                  [Gemm(4096, n, k, ("normal", 0.0, 1.0), ("normal", 0.0, 0.02),
                        5000 + 10 * j + 1, 5000 + 10 * j + 2, out="bf16")

@@ -26,14 +26,16 @@ SFC_ERR_HIP = -4
 SFC_OUT_F32 = 0
 SFC_OUT_BF16 = 1
 
+SFC_CA_AUTO = 0
 TILES = {"auto": 0, "128x128": 1, "256x128": 2, "128x256": 3, "256x256": 4}
+TILE_NAMES = {v: k for k, v in TILES.items()}
 ORDERS = {"hilbert": 0, "row_major": 1}
 SCHEDS = {"interleaved": 0, "block": 1}
 
 # Every symbol include/sfcgemm.h declares.
 EXPORTS = ["sfc_tile_order", "sfc_tile_order_ex", "sfc_gemm", "sfc_gemm_bf16out", "sfc_gemm_ws_size",
-           "sfc_gemm_ex", "sfc_gemm_plan", "sfc_probe_mfma", "sfc_strerror", "sfc_last_error",
-           "sfc_version"]
+           "sfc_gemm_ex", "sfc_gemm_plan", "sfc_gemm_model", "sfc_probe_mfma", "sfc_strerror",
+           "sfc_last_error", "sfc_version"]
 
 
 class SfcError(RuntimeError):
@@ -62,6 +64,9 @@ def _load() -> ctypes.CDLL:
     lib.sfc_gemm_ws_size.restype = sz
     lib.sfc_gemm_plan.argtypes = [i64, i64, i64, i32, i32, ctypes.POINTER(ctypes.c_int64)]
     lib.sfc_gemm_plan.restype = i32
+    lib.sfc_gemm_model.argtypes = [i64, i64, i64, i32, i32, i32, i32, ctypes.POINTER(ctypes.c_int32),
+                                   ctypes.POINTER(ctypes.c_int64)]
+    lib.sfc_gemm_model.restype = i32
     lib.sfc_probe_mfma.argtypes = [i32, i32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]
     lib.sfc_probe_mfma.restype = i32
     lib.sfc_strerror.argtypes = [i32]
@@ -105,6 +110,16 @@ def sfc_gemm_plan(M: int, N: int, K: int, ca_layers: int = 1, tile: str = "auto"
     _check(lib.sfc_gemm_plan(M, N, K, ca_layers, TILES[tile], plan), "sfc_gemm_plan")
     keys = ["BM", "BN", "gm", "gn", "layers", "workgroups", "per_cu"]
     return dict(zip(keys, [int(v) for v in plan]))
+
+
+def sfc_gemm_model(M: int, N: int, K: int, out: str = "f32", ca_layers: int = SFC_CA_AUTO,
+                   tile: str = "auto", num_cus: int = 256, occupancy=(2, 1, 1, 1)) -> dict:
+    """The model's (block shape, layer count) for given device parameters (host only)."""
+    occ = (ctypes.c_int32 * 4)(*occupancy)
+    ch = (ctypes.c_int64 * 3)()
+    _check(lib.sfc_gemm_model(M, N, K, SFC_OUT_BF16 if out == "bf16" else SFC_OUT_F32, ca_layers, TILES[tile],
+                              num_cus, occ, ch), "sfc_gemm_model")
+    return {"tile": TILE_NAMES[int(ch[0])], "layers": int(ch[1]), "clk": int(ch[2])}
 
 
 def sfc_probe_mfma(random_operands: bool = True, iterations: int = 20000) -> dict:

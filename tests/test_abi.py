@@ -50,7 +50,9 @@ def test_version_and_strings(sg):
     (100, 50, 130, 4, 3 * 100 * 50 * 4),  # three K blocks: three layers
     (100, 50, 0, 4, 0),
     (-1, 5, 5, 2, 0),
-    (5, 5, 500, 0, 0),
+    (5, 5, 500, 0, 8 * 5 * 5 * 4),       # SFC_CA_AUTO: bound for the model's largest count, 8
+    (5, 5, 100, 0, 2 * 5 * 5 * 4),       # ... capped at the K blocks
+    (5, 5, 500, -1, 0),
     (5, 5, 500, 65, 0),
 ])
 def test_ws_size(sg, M, N, K, c, want):
@@ -73,12 +75,15 @@ def call_ex(sg, **kw):
     (dict(M=-1), -1), (dict(N=-2), -1), (dict(K=-3), -1),
     (dict(lda=63), -1), (dict(ldb=63), -1), (dict(ldc=63), -1),
     (dict(A=None), -1), (dict(B=None), -1), (dict(C=None), -1),
-    (dict(c=0), -1), (dict(c=65), -1), (dict(out=2), -1),
+    (dict(c=-1), -1), (dict(c=65), -1), (dict(out=2), -1),
     (dict(tile=5), -1), (dict(tile=-1), -1), (dict(order=2), -1), (dict(sched=3), -1),
     (dict(A=4097), -2), (dict(B=8193), -2), (dict(C=16386), -2),
     (dict(M=1 << 31), -2), (dict(K=1 << 31, lda=1 << 31), -2),
     (dict(c=2, K=128, lda=128, ws=1 << 20, wsb=2 * 64 * 64 * 4 - 1), -3),
     (dict(c=2, K=128, lda=128, ws=(1 << 20) + 8, wsb=1 << 20), -2),
+    # SFC_CA_AUTO with a caller workspace: it must hold the largest count the
+    # model picks (8 layers, here capped at the 4 K blocks)
+    (dict(c=0, K=256, lda=256, ws=1 << 20, wsb=4 * 64 * 64 * 4 - 1), -3),
 ])
 def test_invalid_arguments_rejected_before_any_launch(sg, kw, code):
     assert call_ex(sg, **kw) == code
@@ -95,7 +100,7 @@ def test_empty_output_is_a_noop(sg):
 def test_simple_entry_points_validate(sg):
     assert sg.lib.sfc_gemm(4, 4, 4, None, 4, 4096, 4, 8192, 4, 1, None) == -1
     assert sg.lib.sfc_gemm(4, 4, 4, 4096, 4, 4096, 4, 8192, 3, 1, None) == -1
-    assert sg.lib.sfc_gemm_bf16out(4, 4, 4, 4096, 4, 4096, 4, 8192, 4, 0, None) == -1
+    assert sg.lib.sfc_gemm_bf16out(4, 4, 4, 4096, 4, 4096, 4, 8192, 4, -1, None) == -1
 
 
 @pytest.mark.parametrize("gm,gn,order,code", [(0, 4, 0, -1), (4, -1, 0, -1), (4, 4, 7, -1),

@@ -212,3 +212,19 @@ def test_mfma_probe_runs():
     c = sg().sfc_probe_mfma(False, 2000)
     for v in (r, c):
         assert 100.0 < v["tflops"] < 3000.0 and 500.0 < v["mhz"] < 3000.0
+
+
+@pytest.mark.parametrize("M,N,K,out", [(256, 192, 8192, "f32"), (300, 520, 4104, "bf16"), (64, 64, 20000, "f32")])
+def test_auto_layers_match_oracle(M, N, K, out):
+    """SFC_CA_AUTO: the model's block shape and layer count (row f1), checked
+    against the fp64 oracle; on these K-dominant shapes it picks layers."""
+    A, B = operands(M, N, K, 700 + M)
+    C = run_gemm(A, B, M, N, K, out=out, ca_layers=0)
+    Cr, R = oracle(A, B, M, N, K)
+    ocheck.assert_gemm_close(C, Cr, R, f"auto {M}x{N}x{K} {out}")
+    plan = sg().sfc_gemm_plan(M, N, K, 0, "auto")
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    occ = tuple(sg().sfc_gemm_plan(M, N, K, 1, t)["per_cu"] for t in TILES)
+    model = sg().sfc_gemm_model(M, N, K, out="f32", ca_layers=0, num_cus=cus, occupancy=occ)
+    assert (f"{plan['BM']}x{plan['BN']}", plan["layers"]) == (model["tile"], model["layers"])
+    assert plan["layers"] > 1

@@ -95,3 +95,67 @@ def test_gemm_mutant_fails_a_pin(tmp_path, name):
         lib.gemm_ref_rows(0, M, N, K, A.ctypes.data, lda, B.ctypes.data, ldb, C.ctypes.data, R.ctypes.data)
         return C, R
     assert pins.gemm_pin_failures(rows), f"mutant {name} passed every pin"
+
+
+MODEL_SRC = open(os.path.join(ROOT, "oracle", "model.py")).read()
+MODEL_MUTANTS = {
+    "no_patch_sharing": ("t_blk = brgemm_clk(G, gamma, beta / math.sqrt(patch),", "t_blk = brgemm_clk(G, gamma, beta,"),
+    "panel_a_uses_bn": ("BM * BK * 2.0, BK * BN * 2.0)", "BN * BK * 2.0, BK * BN * 2.0)"),
+    "gamma_ignores_occupancy": ("gamma = o / (FLOPS_PER_CLK_CU * RATE[shape])", "gamma = 1 / (FLOPS_PER_CLK_CU * RATE[shape])"),
+    "copies_not_read_back": ("2 * c * M * N * 4 + M * N * out_bytes", "c * M * N * 4 + M * N * out_bytes"),
+    "no_reduction_launch": ("launches = 1 if c == 1 else 2", "launches = 1"),
+    "blocks_not_split": ("blocks = -(-nK // c)", "blocks = nK"),
+    "rounds_floor": ("rounds = -(-tasks // slots)", "rounds = max(1, tasks // slots)"),
+    "eq1_sum": ("return max(G * gamma, beta * (s_a + s_b))", "return G * gamma + beta * (s_a + s_b)"),
+    "ties_keep_last": ("clk <= b_clk + tol and pad < b_pad)", "clk <= b_clk + tol and pad <= b_pad)"),
+}
+
+
+def _model_pins(mod):
+    """The pins of tests/test_oracle_model.py, run on a mutant; returns failures."""
+    fails = []
+    occ = {(128, 128): 2, (256, 128): 1, (128, 256): 1, (256, 256): 1}
+    if abs(mod.brgemm_clk(8388608, 1 / 3031.04, 0.01, 32768, 32768) - 2767.5676) > 1e-3:
+        fails.append("eq1 compute")
+    if abs(mod.brgemm_clk(8388608, 1 / 3031.04, 0.1, 32768, 32768) - 6553.6) > 1e-6:
+        fails.append("eq1 memory")
+    clk, pad = mod.estimate(1024, 1024, 65536, 4, 256, occ, (128, 256), 8)
+    if abs(clk - 248753.89) > 248753.89 * 1e-8 or pad != 256 * 128 * 256:
+        fails.append("worked estimate")
+    for (M, N, K) in [(3000, 7000, 2048), (1024, 4096, 8192), (8192, 512, 65536), (777, 5000, 1000)]:
+        for s in mod.SHAPES:
+            for c in mod.LAYERS:
+                a = mod.estimate(M, N, K, 4, 256, occ, s, c)
+                b = mod.estimate(N, M, K, 4, 256, occ, (s[1], s[0]), c)
+                if abs(a[0] - b[0]) > 1e-12 * abs(a[0]) or a[1] != b[1]:
+                    fails.append("symmetry")
+    if mod.choose(1024, 1024, 65536, out_bytes=4)[1] <= 1:
+        fails.append("k-dominant layers")
+    if mod.choose(8192, 8192, 8192, out_bytes=2)[:2] != ((256, 256), 1):
+        fails.append("square")
+    if mod.choose(512, 512, 128, layers=8)[1] != 2:
+        fails.append("cap")
+    r = mod.choose(0, 0, 64)
+    if r[:2] != ((256, 256), 1) or r[2] != mod.LAUNCH_CLK:
+        fails.append("ties")
+    # worked tie case: the same M x N x K with one layer available twice
+    if mod.choose(512, 512, 64, shape=(128, 128), layers=8)[1] != 1:
+        fails.append("cap to one block")
+    clk, _ = mod.estimate(8192, 8192, 8192, 4, 4096, occ, (128, 256), 1)
+    if abs(clk - 316783.38) > 316783.38 * 1e-8:
+        fails.append("memory-bound worked estimate")
+    return fails
+
+
+@pytest.mark.parametrize("name", sorted(MODEL_MUTANTS))
+def test_model_mutant_fails_a_pin(name):
+    old, new = MODEL_MUTANTS[name]
+    assert old in MODEL_SRC, name
+    mod = types.ModuleType("model_mutant_" + name)
+    exec(compile(MODEL_SRC.replace(old, new, 1), name, "exec"), mod.__dict__)
+    assert _model_pins(mod), f"mutant {name} passed every pin"
+
+
+def test_model_oracle_passes_its_pins():
+    from oracle import model
+    assert _model_pins(model) == []
