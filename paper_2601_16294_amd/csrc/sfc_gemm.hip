@@ -9,8 +9,9 @@
 // fp32 workspace layer that a separate reduction sums.
 //
 // Mapping to the chip:
-//   * one workgroup = 4 waves (2 x 2), each wave owns a (BM/2) x (BN/2)
-//     sub-block held as 16x16 fp32 MFMA accumulators;
+//   * one workgroup = 4 waves (2 x 2; one per SIMD), each wave owns a
+//     (BM/2) x (BN/2) sub-block held as 16x16 fp32 MFMA accumulators; the
+//     fast path can also run 8 waves (2 x 4, two per SIMD) per workgroup;
 //   * the grid is persistent: P workgroups, P = CUs x occupancy, each looping
 //     over tasks.  Hardware deals workgroup b to chiplet (XCD) b % 8; ranks are
 //     renumbered so that each XCD's workgroups hold consecutive ranks, and with
@@ -33,7 +34,10 @@
 //     64-bank LDS;
 //   * bf16 MFMA 16x16x32 with fp32 accumulation (Section III.A's BRGEMM role).
 //     With random operands it holds a higher clock than 32x32x16 for the same
-//     work per clock.
+//     work per clock;
+//   * bf16 output: v_permlane16_swap pairs two fragments so that every lane
+//     stores 8 consecutive columns (16 bytes); a store instruction costs about
+//     the same whatever its width, so this halves the epilogue.
 #include <type_traits>
 #include <utility>
 
@@ -135,22 +139,28 @@ __device__ __forceinline__ void wait_lds_all() { asm volatile("s_waitcnt lgkmcnt
 // The MFMA takes the B fragment as its first operand, so it computes the
 // transposed 16x16 block: lane l ends with row l%16 of the fragment and its 4
 // consecutive columns 4*(l/16) .. +3.
-template <int BM, int BN>
+// NW waves per workgroup in a 2 x (NW/2) grid: 4 waves (one per SIMD) or 8
+// (two per SIMD, so that one wave's MFMAs run while the other issues its reads,
+// loads and waits).
+template <int BM, int BN, int NW>
 struct Tile {
-  static constexpr int WTM = BM / 2, WTN = BN / 2;   // wave sub-block (2 x 2 waves)
-  static constexpr int FM = WTM / 16, FN = WTN / 16; // 16x16 fragments per wave
+  static_assert(NW == 4 || NW == 8, "4 or 8 waves");
+  static constexpr int THREADS = NW * 64;
+  static constexpr int WGN = NW / 2;                  // waves along N
+  static constexpr int WTM = BM / 2, WTN = BN / WGN;  // wave sub-block
+  static constexpr int FM = WTM / 16, FN = WTN / 16;  // 16x16 fragments per wave
   static constexpr int A_ELEMS = BM * kBK, B_ELEMS = kBK * BN;
-  static constexpr int A_CH = BM * kBK / 8 / kThreads;   // 16-byte chunks per thread
-  static constexpr int B_CH = kBK * BN / 8 / kThreads;
+  static constexpr int A_CH = BM * kBK / 8 / THREADS;   // 16-byte chunks per thread
+  static constexpr int B_CH = kBK * BN / 8 / THREADS;
 };
 
-template <int BM, int BN>
-using Acc = f32x4[Tile<BM, BN>::FM][Tile<BM, BN>::FN];
+template <int BM, int BN, int NW>
+using Acc = f32x4[Tile<BM, BN, NW>::FM][Tile<BM, BN, NW>::FN];
 
-template <int BM, int BN>
+template <int BM, int BN, int NW>
 struct Frags {
-  bf16x8 a[Tile<BM, BN>::FM];
-  bf16x8 b[Tile<BM, BN>::FN];
+  bf16x8 a[Tile<BM, BN, NW>::FM];
+  bf16x8 b[Tile<BM, BN, NW>::FN];
 };
 
 // Per-lane LDS element offsets of the fragment reads of one 32-deep step:
@@ -183,10 +193,10 @@ __device__ __forceinline__ bf16x8 read_b_pair(const uint16_t* p, int half_stride
 
 // All operand fragments of one 32-deep step from an A block [BM][64] (step
 // ks) and a B buffer [..][BN] (rows kbase .. kbase+31).
-template <int BM, int BN>
+template <int BM, int BN, int NW>
 __device__ __forceinline__ void load_frags(const uint16_t* As, const uint16_t* Bs, int wm, int wn,
-                                           int lane, int ks, int kbase, Frags<BM, BN>& f) {
-  using T = Tile<BM, BN>;
+                                           int lane, int ks, int kbase, Frags<BM, BN, NW>& f) {
+  using T = Tile<BM, BN, NW>;
   const int ao = a_frag_off(wm * T::WTM, lane, ks);
 #pragma unroll
   for (int i = 0; i < T::FM; ++i) f.a[i] = *reinterpret_cast<const bf16x8*>(As + ao + i * 16 * kBK);
@@ -195,9 +205,9 @@ __device__ __forceinline__ void load_frags(const uint16_t* As, const uint16_t* B
 }
 
 // acc += one 32-deep step.
-template <int BM, int BN>
-__device__ __forceinline__ void mma_step(const Frags<BM, BN>& cur, Acc<BM, BN>& acc) {
-  using T = Tile<BM, BN>;
+template <int BM, int BN, int NW>
+__device__ __forceinline__ void mma_step(const Frags<BM, BN, NW>& cur, Acc<BM, BN, NW>& acc) {
+  using T = Tile<BM, BN, NW>;
 #pragma unroll
   for (int i = 0; i < T::FM; ++i)
 #pragma unroll
@@ -219,14 +229,14 @@ __device__ __forceinline__ void mma_step(const Frags<BM, BN>& cur, Acc<BM, BN>& 
 // Every instruction of the loop counts: with one wave per SIMD a wave issues
 // at most one instruction per four clocks, so the loop keeps its other work
 // (LDS reads, loads, address arithmetic) to a few instructions per MFMA,
-// spread evenly.
+// spread evenly.  (With 8 waves two waves share a SIMD and interleave.)
 constexpr int kSK = 32;        // K depth of one B stage (one MFMA step)
 constexpr int kBias = 4096;    // bytes; keeps every biased voffset positive
 
 // The loads of block b+D are issued during block b (prefetch depth D): the A
 // ring has D+1 block slots, the B ring 2D stage slots.  D = 3 where the LDS
 // holds that at the same occupancy (128x256: exactly 160 KiB), else 2.
-template <int BM, int BN>
+template <int BM, int BN, int NW>
 struct Ring {
   static constexpr int A_BLK = BM * kBK;                 // elements of one A block
   static constexpr int B_STG = kSK * BN;                 // elements of one B stage
@@ -234,8 +244,8 @@ struct Ring {
   static constexpr int D = (BM == 128 && BN == 256) ? 3 : 2;
   static constexpr int NA = D + 1, NB = 2 * D;           // A block slots, B stage slots
   static constexpr int B_OFF = NA * A_BYTES;             // byte offset of the B slots
-  static constexpr int APB = A_BYTES / 1024 / 4;         // A loads per wave per block
-  static constexpr int BPW = B_BYTES / 1024 / 4;         // B loads per wave per stage
+  static constexpr int APB = A_BYTES / 1024 / NW;        // A loads per wave per block
+  static constexpr int BPW = B_BYTES / 1024 / NW;        // B loads per wave per stage
   static constexpr int ELEMS = NA * A_BLK + NB * B_STG;
   // loads younger than block b+1's, when block b's barrier waits for it
   static constexpr int IN_FLIGHT = (D - 2) * (APB + 2 * BPW) + APB;
@@ -272,10 +282,10 @@ __device__ __forceinline__ i32x4 make_rsrc_addr(uint64_t a, uint32_t num_records
 }
 
 // Per-lane, per-task load offsets (bytes, biased).
-template <int BM, int BN>
+template <int BM, int BN, int NW>
 struct RingLanes {
-  int a_voff[Ring<BM, BN>::APB];
-  int b_voff[Ring<BM, BN>::BPW];
+  int a_voff[Ring<BM, BN, NW>::APB];
+  int b_voff[Ring<BM, BN, NW>::BPW];
 };
 
 // K index (within a block) at which A load j of this lane starts.
@@ -284,10 +294,10 @@ __device__ __forceinline__ int a_load_k(int wave, int apb, int j, int lane) {
   return ((lane & 7) ^ ((row >> 1) & 7)) * 8;
 }
 
-template <int BM, int BN>
+template <int BM, int BN, int NW>
 __device__ __forceinline__ void ring_lanes(const GemmParams& p, int64_t m0, int64_t n0, int wave,
-                                           int lane, RingLanes<BM, BN>& L) {
-  using R = Ring<BM, BN>;
+                                           int lane, RingLanes<BM, BN, NW>& L) {
+  using R = Ring<BM, BN, NW>;
 #pragma unroll
   for (int j = 0; j < R::APB; ++j) {
     const int row = (wave * R::APB + j) * 8 + (lane >> 3);
@@ -305,18 +315,18 @@ __device__ __forceinline__ void ring_lanes(const GemmParams& p, int64_t m0, int6
 
 // Turn the A lanes whose load starts at a K index >= kin (within the block)
 // into out-of-range lanes, for the loads of a block that runs past K.
-template <int BM, int BN>
-__device__ __forceinline__ void mask_a_lanes(RingLanes<BM, BN>& L, int wave, int lane, int64_t kin) {
-  using R = Ring<BM, BN>;
+template <int BM, int BN, int NW>
+__device__ __forceinline__ void mask_a_lanes(RingLanes<BM, BN, NW>& L, int wave, int lane, int64_t kin) {
+  using R = Ring<BM, BN, NW>;
 #pragma unroll
   for (int j = 0; j < R::APB; ++j)
     if (a_load_k(wave, R::APB, j, lane) >= kin) L.a_voff[j] = kOobOffset;
 }
 
 // The same without a branch: masks only when `on` (wave-uniform).
-template <int BM, int BN>
-__device__ __forceinline__ void mask_a_lanes_if(RingLanes<BM, BN>& L, int wave, int lane, int64_t kin, bool on) {
-  using R = Ring<BM, BN>;
+template <int BM, int BN, int NW>
+__device__ __forceinline__ void mask_a_lanes_if(RingLanes<BM, BN, NW>& L, int wave, int lane, int64_t kin, bool on) {
+  using R = Ring<BM, BN, NW>;
 #pragma unroll
   for (int j = 0; j < R::APB; ++j)
     L.a_voff[j] = (on && a_load_k(wave, R::APB, j, lane) >= kin) ? kOobOffset : L.a_voff[j];
@@ -326,15 +336,15 @@ __device__ __forceinline__ void mask_a_lanes_if(RingLanes<BM, BN>& L, int wave, 
 // a_rd[ks] + i*2048 within its slot; the two halves of B fragment j at
 // b_rd[j] and b_rd[j] + 8*BN in B slot 0 (LDS byte addresses; slot s adds
 // s times the slot size, an immediate offset of the read).
-template <int BM, int BN>
+template <int BM, int BN, int NW>
 struct ReadOffsets {
   uint32_t a_rd[2];
-  uint32_t b_rd[Tile<BM, BN>::FN];
+  uint32_t b_rd[Tile<BM, BN, NW>::FN];
 };
 
-template <int BM, int BN>
-__device__ __forceinline__ void read_offsets(int wm, int wn, int lane, uint32_t b_ring, ReadOffsets<BM, BN>& o) {
-  using T = Tile<BM, BN>;
+template <int BM, int BN, int NW>
+__device__ __forceinline__ void read_offsets(int wm, int wn, int lane, uint32_t b_ring, ReadOffsets<BM, BN, NW>& o) {
+  using T = Tile<BM, BN, NW>;
 #pragma unroll
   for (int ks = 0; ks < 2; ++ks) o.a_rd[ks] = (uint32_t)(a_frag_off(wm * T::WTM, lane, ks) * 2);
 #pragma unroll
@@ -343,10 +353,10 @@ __device__ __forceinline__ void read_offsets(int wm, int wn, int lane, uint32_t 
 
 // Read item t of a step, in the order the next step's MFMAs consume them:
 // A0, B0, B1, .., B(FN-1), A1, .., A(FM-1).
-template <int BM, int BN>
+template <int BM, int BN, int NW>
 __device__ __forceinline__ void read_item(int t, uint32_t a_base, uint32_t b_slot, const uint32_t* b_rd,
-                                          Frags<BM, BN>& f) {
-  using T = Tile<BM, BN>;
+                                          Frags<BM, BN, NW>& f) {
+  using T = Tile<BM, BN, NW>;
   if (t == 0 || t > T::FN) {
     const int i = t == 0 ? 0 : t - T::FN;
     f.a[i] = *(lds_bf16x8*)(uintptr_t)(a_base + (uint32_t)(i * 16 * kBK * 2));
@@ -369,8 +379,8 @@ struct SlotDma {
 };
 
 // Load pair q (loads 2q, 2q+1) of an A block (OP 1) or a B stage (OP 2).
-template <int BM, int BN, int OP, int Q>
-__device__ __forceinline__ void dma_pair(const SlotDma& d, const RingLanes<BM, BN>& L) {
+template <int BM, int BN, int NW, int OP, int Q>
+__device__ __forceinline__ void dma_pair(const SlotDma& d, const RingLanes<BM, BN, NW>& L) {
   constexpr int j = 2 * Q;
   if constexpr (OP == 1)
     dma16_pair<(j & 3) * 1024>(d.rsrc, d.m0 + (uint32_t)((j >> 2) * 4096), L.a_voff[j], L.a_voff[j + 1]);
@@ -379,11 +389,11 @@ __device__ __forceinline__ void dma_pair(const SlotDma& d, const RingLanes<BM, B
 }
 
 // All loads of an A block (OP 1) or a B stage (OP 2).
-template <int BM, int BN, int OP>
-__device__ __forceinline__ void dma_all(const SlotDma& d, const RingLanes<BM, BN>& L) {
-  using R = Ring<BM, BN>;
+template <int BM, int BN, int NW, int OP>
+__device__ __forceinline__ void dma_all(const SlotDma& d, const RingLanes<BM, BN, NW>& L) {
+  using R = Ring<BM, BN, NW>;
   [&]<int... q>(std::integer_sequence<int, q...>) {
-    (dma_pair<BM, BN, OP, q>(d, L), ...);
+    (dma_pair<BM, BN, NW, OP, q>(d, L), ...);
   }(std::make_integer_sequence<int, (OP == 1 ? R::APB : R::BPW) / 2>{});
 }
 
@@ -397,19 +407,21 @@ __device__ __forceinline__ void dma_all(const SlotDma& d, const RingLanes<BM, BN
 //   loads:  each load pair becomes three operations (set M0, load, load) in
 //           consecutive groups from evenly spaced starting groups, so that the
 //           MFMA between M0 and the first load covers the wait M0 needs.
-template <int BM, int BN, int OP>
+template <int BM, int BN, int NW, int OP>
 struct StepPlan {
-  using T = Tile<BM, BN>;
+  using T = Tile<BM, BN, NW>;
   static constexpr int G = T::FM * T::FN;
   static constexpr int NR = T::FM + 2 * T::FN;
-  static constexpr int NP0 = OP == 1 ? Ring<BM, BN>::APB / 2 : Ring<BM, BN>::BPW / 2;   // pairs from d0
-  static constexpr int NP1 = OP == 1 ? 0 : Ring<BM, BN>::BPW / 2;                      // pairs from d1
+  static constexpr int NP0 = OP == 1 ? Ring<BM, BN, NW>::APB / 2 : Ring<BM, BN, NW>::BPW / 2;   // pairs from d0
+  static constexpr int NP1 = OP == 1 ? 0 : Ring<BM, BN, NW>::BPW / 2;                      // pairs from d1
   static constexpr int NP = NP0 + NP1;
   static constexpr int ND = 3 * NP;
   // the B step opens with G0 groups of MFMAs alone and then waits at the
   // block's barrier: those MFMAs need nothing the barrier publishes, and they
-  // keep the matrix core busy while the waves meet
-  static constexpr int G0 = OP == 2 ? 2 : 0;
+  // keep the matrix core busy while the waves meet and while the A step's last
+  // fragment reads (which the barrier waits for) complete; steps of 32 or more
+  // MFMAs open with 4 (measured best of 2, 4, 6, 8), shorter ones with 2
+  static constexpr int G0 = OP == 2 ? (T::FM * T::FN >= 32 ? 4 : 2) : 0;
   static constexpr int read_group(int r) { return G0 + (r * (G - G0)) / NR; }
   static constexpr int dma_group(int o) {
     int g = G0 - 1;
@@ -422,7 +434,7 @@ struct StepPlan {
   // groups that issue neither a read nor a load operation (nor, in the A
   // step, one of the K-mask selects of the first APB groups)
   static constexpr bool busy(int g) {
-    if (OP == 1 && g < Ring<BM, BN>::APB) return true;
+    if (OP == 1 && g < Ring<BM, BN, NW>::APB) return true;
     for (int r = 0; r < NR; ++r)
       if (read_group(r) == g) return true;
     for (int o = 0; o < ND; ++o)
@@ -449,16 +461,16 @@ struct StepPlan {
 };
 
 // Per-step state of the split B reads: address and low half of each fragment.
-template <int BM, int BN>
+template <int BM, int BN, int NW>
 struct BReads {
-  uint32_t addr[Tile<BM, BN>::FN];
-  i16x4 lo[Tile<BM, BN>::FN];
+  uint32_t addr[Tile<BM, BN, NW>::FN];
+  i16x4 lo[Tile<BM, BN, NW>::FN];
 };
 
-template <int BM, int BN, int OP, int r>
-__device__ __forceinline__ void step_read(uint32_t a_base, uint32_t b_slot, const uint32_t* b_rd, BReads<BM, BN>& br,
-                                          Frags<BM, BN>& nxt) {
-  using T = Tile<BM, BN>;
+template <int BM, int BN, int NW, int OP, int r>
+__device__ __forceinline__ void step_read(uint32_t a_base, uint32_t b_slot, const uint32_t* b_rd, BReads<BM, BN, NW>& br,
+                                          Frags<BM, BN, NW>& nxt) {
+  using T = Tile<BM, BN, NW>;
   if constexpr (r == 0 || r > 2 * T::FN) {
     constexpr int i = r == 0 ? 0 : r - 2 * T::FN;
     nxt.a[i] = *(lds_bf16x8*)(uintptr_t)(a_base + (uint32_t)(i * 16 * kBK * 2));
@@ -475,18 +487,18 @@ __device__ __forceinline__ void step_read(uint32_t a_base, uint32_t b_slot, cons
   }
 }
 
-template <int BM, int BN, int OP, int g, int... r>
+template <int BM, int BN, int NW, int OP, int g, int... r>
 __device__ __forceinline__ void group_reads(uint32_t a_base, uint32_t b_slot, const uint32_t* b_rd,
-                                            BReads<BM, BN>& br, Frags<BM, BN>& nxt, std::integer_sequence<int, r...>) {
-  using P = StepPlan<BM, BN, OP>;
-  ((void)(P::read_group(r) == g ? (step_read<BM, BN, OP, r>(a_base, b_slot, b_rd, br, nxt), 0) : 0), ...);
+                                            BReads<BM, BN, NW>& br, Frags<BM, BN, NW>& nxt, std::integer_sequence<int, r...>) {
+  using P = StepPlan<BM, BN, NW, OP>;
+  ((void)(P::read_group(r) == g ? (step_read<BM, BN, NW, OP, r>(a_base, b_slot, b_rd, br, nxt), 0) : 0), ...);
 }
 
 // Load operation o of a step: o = 3q + k for load pair q (k 0: set M0, k 1
 // and 2: the pair's loads).
-template <int BM, int BN, int OP, int o>
-__device__ __forceinline__ void step_dma(const SlotDma& d0, const SlotDma& d1, const RingLanes<BM, BN>& L) {
-  using P = StepPlan<BM, BN, OP>;
+template <int BM, int BN, int NW, int OP, int o>
+__device__ __forceinline__ void step_dma(const SlotDma& d0, const SlotDma& d1, const RingLanes<BM, BN, NW>& L) {
+  using P = StepPlan<BM, BN, NW, OP>;
   constexpr int q = o / 3, k = o % 3;
   constexpr bool first = q < P::NP0;
   constexpr int qq = first ? q : q - P::NP0;
@@ -503,20 +515,20 @@ __device__ __forceinline__ void step_dma(const SlotDma& d0, const SlotDma& d1, c
   }
 }
 
-template <int BM, int BN, int OP, int g, int... o>
-__device__ __forceinline__ void group_dma(const SlotDma& d0, const SlotDma& d1, const RingLanes<BM, BN>& L,
+template <int BM, int BN, int NW, int OP, int g, int... o>
+__device__ __forceinline__ void group_dma(const SlotDma& d0, const SlotDma& d1, const RingLanes<BM, BN, NW>& L,
                                           std::integer_sequence<int, o...>) {
-  using P = StepPlan<BM, BN, OP>;
-  ((void)(P::dma_group(o) == g ? (step_dma<BM, BN, OP, o>(d0, d1, L), 0) : 0), ...);
+  using P = StepPlan<BM, BN, NW, OP>;
+  ((void)(P::dma_group(o) == g ? (step_dma<BM, BN, NW, OP, o>(d0, d1, L), 0) : 0), ...);
 }
 
-template <int BM, int BN, int OP, int g, typename X>
-__device__ __forceinline__ void ring_group(Acc<BM, BN>& acc, const Frags<BM, BN>& cur, Frags<BM, BN>& nxt,
+template <int BM, int BN, int NW, int OP, int g, typename X>
+__device__ __forceinline__ void ring_group(Acc<BM, BN, NW>& acc, const Frags<BM, BN, NW>& cur, Frags<BM, BN, NW>& nxt,
                                            uint32_t a_base, uint32_t b_slot, const uint32_t* b_rd,
-                                           BReads<BM, BN>& br, const SlotDma& d0, const SlotDma& d1,
-                                           const RingLanes<BM, BN>& L, X& ex) {
-  using T = Tile<BM, BN>;
-  using P = StepPlan<BM, BN, OP>;
+                                           BReads<BM, BN, NW>& br, const SlotDma& d0, const SlotDma& d1,
+                                           const RingLanes<BM, BN, NW>& L, X& ex) {
+  using T = Tile<BM, BN, NW>;
+  using P = StepPlan<BM, BN, NW, OP>;
   constexpr int i = g / T::FN, j = g % T::FN;
   acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(cur.b[j], cur.a[i], acc[i][j], 0, 0, 0);
   if constexpr (OP == 2 && g == P::G0) {
@@ -525,22 +537,22 @@ __device__ __forceinline__ void ring_group(Acc<BM, BN>& acc, const Frags<BM, BN>
     // every wave's reads issued in the A step are done (among them the last
     // reads of the B slot this step loads into, and of the A slot the next A
     // step loads into)
-    wait_vmem_at_most<Ring<BM, BN>::IN_FLIGHT>();
+    wait_vmem_at_most<Ring<BM, BN, NW>::IN_FLIGHT>();
     wait_lds_all();
     __syncthreads();
   }
-  group_reads<BM, BN, OP, g>(a_base, b_slot, b_rd, br, nxt, std::make_integer_sequence<int, P::NR>{});
-  group_dma<BM, BN, OP, g>(d0, d1, L, std::make_integer_sequence<int, P::ND>{});
+  group_reads<BM, BN, NW, OP, g>(a_base, b_slot, b_rd, br, nxt, std::make_integer_sequence<int, P::NR>{});
+  group_dma<BM, BN, NW, OP, g>(d0, d1, L, std::make_integer_sequence<int, P::ND>{});
   ex.template operator()<g>();
   __builtin_amdgcn_sched_barrier(0);
 }
 
-template <int BM, int BN, int OP, typename X, int... g>
-__device__ __forceinline__ void ring_groups(Acc<BM, BN>& acc, const Frags<BM, BN>& cur, Frags<BM, BN>& nxt,
+template <int BM, int BN, int NW, int OP, typename X, int... g>
+__device__ __forceinline__ void ring_groups(Acc<BM, BN, NW>& acc, const Frags<BM, BN, NW>& cur, Frags<BM, BN, NW>& nxt,
                                             uint32_t a_base, uint32_t b_slot, const uint32_t* b_rd,
-                                            BReads<BM, BN>& br, const SlotDma& d0, const SlotDma& d1,
-                                            const RingLanes<BM, BN>& L, X& ex, std::integer_sequence<int, g...>) {
-  (ring_group<BM, BN, OP, g>(acc, cur, nxt, a_base, b_slot, b_rd, br, d0, d1, L, ex), ...);
+                                            BReads<BM, BN, NW>& br, const SlotDma& d0, const SlotDma& d1,
+                                            const RingLanes<BM, BN, NW>& L, X& ex, std::integer_sequence<int, g...>) {
+  (ring_group<BM, BN, NW, OP, g>(acc, cur, nxt, a_base, b_slot, b_rd, br, d0, d1, L, ex), ...);
 }
 
 // One 32-deep step with a fixed instruction order (the plan above): MFMAs of
@@ -549,14 +561,14 @@ __device__ __forceinline__ void ring_groups(Acc<BM, BN>& acc, const Frags<BM, BN
 // (ex.operator()<g>() runs in group g).  The groups are generated as
 // straight-line code (a loop this long is not always unrolled, and the
 // accumulators must stay in registers).
-template <int BM, int BN, int OP, typename X>
-__device__ __forceinline__ void ring_step(Acc<BM, BN>& acc, const Frags<BM, BN>& cur, Frags<BM, BN>& nxt,
-                                          uint32_t a_base, uint32_t b_slot, const ReadOffsets<BM, BN>& o,
-                                          const SlotDma& d0, const SlotDma& d1, const RingLanes<BM, BN>& L,
+template <int BM, int BN, int NW, int OP, typename X>
+__device__ __forceinline__ void ring_step(Acc<BM, BN, NW>& acc, const Frags<BM, BN, NW>& cur, Frags<BM, BN, NW>& nxt,
+                                          uint32_t a_base, uint32_t b_slot, const ReadOffsets<BM, BN, NW>& o,
+                                          const SlotDma& d0, const SlotDma& d1, const RingLanes<BM, BN, NW>& L,
                                           X&& ex) {
-  using T = Tile<BM, BN>;
-  BReads<BM, BN> br;
-  ring_groups<BM, BN, OP>(acc, cur, nxt, a_base, b_slot, o.b_rd, br, d0, d1, L, ex,
+  using T = Tile<BM, BN, NW>;
+  BReads<BM, BN, NW> br;
+  ring_groups<BM, BN, NW, OP>(acc, cur, nxt, a_base, b_slot, o.b_rd, br, d0, d1, L, ex,
                           std::make_integer_sequence<int, T::FM * T::FN>{});
 }
 
@@ -602,14 +614,14 @@ __device__ __forceinline__ uint32_t b_stage_limit(const RingAddr& ra, int x) {
 // outside the B descriptors' ranges and read zeros; A block nb-1 is loaded with
 // its lanes past K masked (selects on the first groups of the step that issues
 // those loads, or in the prologue when nb <= D).
-template <int BM, int BN>
+template <int BM, int BN, int NW>
 __device__ __forceinline__ void main_loop_ring(const RingAddr& ra, int nb, int64_t kin_last,
-                                               const ReadOffsets<BM, BN>& o, RingLanes<BM, BN>& L, int lane,
-                                               Acc<BM, BN>& acc) {
-  using R = Ring<BM, BN>;
-  using T = Tile<BM, BN>;
-  using P1 = StepPlan<BM, BN, 1>;
-  using P2 = StepPlan<BM, BN, 2>;
+                                               const ReadOffsets<BM, BN, NW>& o, RingLanes<BM, BN, NW>& L, int lane,
+                                               Acc<BM, BN, NW>& acc) {
+  using R = Ring<BM, BN, NW>;
+  using T = Tile<BM, BN, NW>;
+  using P1 = StepPlan<BM, BN, NW, 1>;
+  using P2 = StepPlan<BM, BN, NW, 2>;
   constexpr int D = R::D;
   constexpr uint32_t BB = (uint32_t)R::B_BYTES;
   const int wave = ra.wave;
@@ -633,15 +645,15 @@ __device__ __forceinline__ void main_loop_ring(const RingAddr& ra, int nb, int64
   // B slots 2k, 2k+1), then wait for block 0.  Depth 2 loads block 1 only when
   // there is one; deeper rings load blocks past K with empty ranges.
   if constexpr (D == 2) {
-    if (masked && nb == 1) mask_a_lanes<BM, BN>(L, wave, lane, kin_last);
-    dma_all<BM, BN, 1>(a_dma(ra.a0, 0, kOobOffset), L);
-    dma_all<BM, BN, 2>(b_dma(ra.b0, 0, 0), L);
-    dma_all<BM, BN, 2>(b_dma(ra.b0 + ra.b_step, 1, 1), L);
+    if (masked && nb == 1) mask_a_lanes<BM, BN, NW>(L, wave, lane, kin_last);
+    dma_all<BM, BN, NW, 1>(a_dma(ra.a0, 0, kOobOffset), L);
+    dma_all<BM, BN, NW, 2>(b_dma(ra.b0, 0, 0), L);
+    dma_all<BM, BN, NW, 2>(b_dma(ra.b0 + ra.b_step, 1, 1), L);
     if (nb > 1) {
-      if (masked && nb == 2) mask_a_lanes<BM, BN>(L, wave, lane, kin_last);
-      dma_all<BM, BN, 1>(a_dma(ra.a0 + kBK * 2, 1, kOobOffset), L);
-      dma_all<BM, BN, 2>(b_dma(ra.b0 + 2 * ra.b_step, 2, 2), L);
-      dma_all<BM, BN, 2>(b_dma(ra.b0 + 3 * ra.b_step, 3, 3), L);
+      if (masked && nb == 2) mask_a_lanes<BM, BN, NW>(L, wave, lane, kin_last);
+      dma_all<BM, BN, NW, 1>(a_dma(ra.a0 + kBK * 2, 1, kOobOffset), L);
+      dma_all<BM, BN, NW, 2>(b_dma(ra.b0 + 2 * ra.b_step, 2, 2), L);
+      dma_all<BM, BN, NW, 2>(b_dma(ra.b0 + 3 * ra.b_step, 3, 3), L);
       wait_vmem_at_most<R::APB + 2 * R::BPW>();
     } else {
       wait_vmem_at_most<0>();
@@ -649,16 +661,16 @@ __device__ __forceinline__ void main_loop_ring(const RingAddr& ra, int nb, int64
   } else {
 #pragma unroll
     for (int k = 0; k < D; ++k) {
-      if (masked) mask_a_lanes_if<BM, BN>(L, wave, lane, kin_last, k == nb - 1);
-      dma_all<BM, BN, 1>(a_dma(ra.a0 + (uint64_t)k * (kBK * 2), k, k < nb ? (uint32_t)kOobOffset : 0u), L);
-      dma_all<BM, BN, 2>(b_dma(ra.b0 + (uint64_t)(2 * k) * ra.b_step, 2 * k, 2 * k), L);
-      dma_all<BM, BN, 2>(b_dma(ra.b0 + (uint64_t)(2 * k + 1) * ra.b_step, 2 * k + 1, 2 * k + 1), L);
+      if (masked) mask_a_lanes_if<BM, BN, NW>(L, wave, lane, kin_last, k == nb - 1);
+      dma_all<BM, BN, NW, 1>(a_dma(ra.a0 + (uint64_t)k * (kBK * 2), k, k < nb ? (uint32_t)kOobOffset : 0u), L);
+      dma_all<BM, BN, NW, 2>(b_dma(ra.b0 + (uint64_t)(2 * k) * ra.b_step, 2 * k, 2 * k), L);
+      dma_all<BM, BN, NW, 2>(b_dma(ra.b0 + (uint64_t)(2 * k + 1) * ra.b_step, 2 * k + 1, 2 * k + 1), L);
     }
     wait_vmem_at_most<(D - 1) * (R::APB + 2 * R::BPW)>();
   }
   __syncthreads();
 
-  Frags<BM, BN> f0, f1;
+  Frags<BM, BN, NW> f0, f1;
   {
     const uint32_t as = ra.lds0 + o.a_rd[0];
     // B slot 0, as an opaque register value: with a literal 0 the compiler
@@ -669,7 +681,7 @@ __device__ __forceinline__ void main_loop_ring(const RingAddr& ra, int nb, int64
     // first MFMAs wait only for their own operands on either path into the loop
 #pragma unroll
     for (int t = 0; t < T::FM + T::FN; ++t) {
-      read_item<BM, BN>(t, as, bs0, o.b_rd, f0);
+      read_item<BM, BN, NW>(t, as, bs0, o.b_rd, f0);
       __builtin_amdgcn_sched_barrier(0);
     }
   }
@@ -694,7 +706,7 @@ __device__ __forceinline__ void main_loop_ring(const RingAddr& ra, int nb, int64
   uint32_t lim0, lim1;
   uint64_t b_nx1;
   for (int b = 0; b < nb; ++b) {
-    ring_step<BM, BN, 1>(acc, f0, f1, ra.lds0 + la0 + o.a_rd[1], lb1, o, da, da, L, [&]<int g>() {
+    ring_step<BM, BN, NW, 1>(acc, f0, f1, ra.lds0 + la0 + o.a_rd[1], lb1, o, da, da, L, [&]<int g>() {
       if constexpr (g < R::APB) {
         if (mnow && mk[g]) L.a_voff[g] = kOobOffset;
       }
@@ -708,7 +720,7 @@ __device__ __forceinline__ void main_loop_ring(const RingAddr& ra, int nb, int64
       if constexpr (g == P1::stage_group(4, 6)) b_nx1 = b_nx + ra.b_step;
       if constexpr (g == P1::stage_group(5, 6)) db1.rsrc = make_rsrc_addr(b_nx1, lim1);
     });
-    ring_step<BM, BN, 2>(acc, f1, f0, ra.lds0 + la1 + o.a_rd[0], lb2, o, db0, db1, L, [&]<int g>() {
+    ring_step<BM, BN, NW, 2>(acc, f1, f0, ra.lds0 + la1 + o.a_rd[0], lb2, o, db0, db1, L, [&]<int g>() {
       if constexpr (g == P2::stage_group(0, 5)) {
         const uint32_t t = la0;
         la0 = la1;
@@ -756,23 +768,23 @@ __device__ __forceinline__ void main_loop_ring(const RingAddr& ra, int nb, int64
 }
 
 // ---- main loop, general path: element loads staged in registers ---------------------------
-template <int BM, int BN>
+template <int BM, int BN, int NW>
 __device__ __forceinline__ void main_loop_staged(const GemmParams& p, uint16_t* smem, int64_t m0,
-                                                 int64_t n0, int kt0, int kt1, int tid, Acc<BM, BN>& acc) {
-  using T = Tile<BM, BN>;
+                                                 int64_t n0, int kt0, int kt1, int tid, Acc<BM, BN, NW>& acc) {
+  using T = Tile<BM, BN, NW>;
   const int lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / T::WGN, wn = wave % T::WGN;
   u32x4 ra[T::A_CH], rb[T::B_CH];
   auto load_blocks = [&](int kt) {
     const int64_t k0 = (int64_t)kt * kBK;
 #pragma unroll
     for (int i = 0; i < T::A_CH; ++i) {
-      const int q = tid + kThreads * i;
+      const int q = tid + T::THREADS * i;
       ra[i] = load_chunk<false>(p.A, p.lda, m0 + (q >> 3), k0 + (q & 7) * 8, p.M, p.K);
     }
 #pragma unroll
     for (int i = 0; i < T::B_CH; ++i) {
-      const int q = tid + kThreads * i;
+      const int q = tid + T::THREADS * i;
       rb[i] = load_chunk<false>(p.B, p.ldb, k0 + q / (BN / 8), n0 + (q % (BN / 8)) * 8, p.K, p.N);
     }
   };
@@ -781,12 +793,12 @@ __device__ __forceinline__ void main_loop_staged(const GemmParams& p, uint16_t* 
     uint16_t* Bs = As + T::A_ELEMS;
 #pragma unroll
     for (int i = 0; i < T::A_CH; ++i) {
-      const int q = tid + kThreads * i;
+      const int q = tid + T::THREADS * i;
       *reinterpret_cast<u32x4*>(As + a_off(q >> 3, q & 7)) = ra[i];
     }
 #pragma unroll
     for (int i = 0; i < T::B_CH; ++i) {
-      const int q = tid + kThreads * i;
+      const int q = tid + T::THREADS * i;
       *reinterpret_cast<u32x4*>(Bs + b_off<BN>(q / (BN / 8), (q % (BN / 8)) * 8)) = rb[i];
     }
   };
@@ -800,9 +812,9 @@ __device__ __forceinline__ void main_loop_staged(const GemmParams& p, uint16_t* 
     const uint16_t* As = smem + buf * (T::A_ELEMS + T::B_ELEMS);
 #pragma unroll
     for (int ks = 0; ks < kBK / 32; ++ks) {
-      Frags<BM, BN> f;
-      load_frags<BM, BN>(As, As + T::A_ELEMS, wm, wn, lane, ks, 32 * ks, f);
-      mma_step<BM, BN>(f, acc);
+      Frags<BM, BN, NW> f;
+      load_frags<BM, BN, NW>(As, As + T::A_ELEMS, wm, wn, lane, ks, 32 * ks, f);
+      mma_step<BM, BN, NW>(f, acc);
     }
     if (more) store_blocks(buf ^ 1);
     __syncthreads();
@@ -812,14 +824,47 @@ __device__ __forceinline__ void main_loop_staged(const GemmParams& p, uint16_t* 
 // ---- epilogue ---------------------------------------------------------------------------------
 // Fragment (i, j) of the wave: lane l holds row 16i + l%16 and columns
 // 16j + 4*(l/16) .. +3 of the wave's sub-block.
-template <int BM, int BN, bool OUT_BF16>
-__device__ __forceinline__ void store_tile(const GemmParams& p, const Acc<BM, BN>& acc, int64_t m0, int64_t n0,
-                                           int64_t lstride, int wm, int wn, int lane, bool fast) {
-  using T = Tile<BM, BN>;
+// Two bf16-packed fragments (j, j+1) of one 16-row strip, each lane holding 4
+// consecutive columns (two dwords) of each, rearranged so that each lane holds
+// 8 consecutive columns of one of them: v_permlane16_swap exchanges the odd
+// 16-lane rows of its first operand with the even rows of its second, so lane
+// group q ends with columns 16*(q&1) + 8*(q>>1) .. +7 of the pair.
+__device__ __forceinline__ u32x4 pair_to_row8(const f32x4& x, const f32x4& y) {
+  const bf16x4 xb = {(__bf16)x[0], (__bf16)x[1], (__bf16)x[2], (__bf16)x[3]};
+  const bf16x4 yb = {(__bf16)y[0], (__bf16)y[1], (__bf16)y[2], (__bf16)y[3]};
+  typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+  const u32x2 xw = __builtin_bit_cast(u32x2, xb), yw = __builtin_bit_cast(u32x2, yb);
+  const auto s0 = __builtin_amdgcn_permlane16_swap(xw[0], yw[0], false, false);
+  const auto s1 = __builtin_amdgcn_permlane16_swap(xw[1], yw[1], false, false);
+  return u32x4{s0[0], s1[0], s0[1], s1[1]};
+}
+
+template <int BM, int BN, int NW, bool OUT_BF16>
+__device__ __forceinline__ void store_tile(const GemmParams& p, const Acc<BM, BN, NW>& acc, int64_t m0, int64_t n0,
+                                           int64_t lstride, int wm, int wn, int lane, bool fast, bool fast16) {
+  using T = Tile<BM, BN, NW>;
   typedef typename std::conditional<OUT_BF16, __bf16, float>::type OutT;
   OutT* out = reinterpret_cast<OutT*>(p.out) + lstride;
   const int64_t r0 = m0 + wm * T::WTM + (lane & 15);
   const int64_t c0 = n0 + wn * T::WTN + 4 * (lane >> 4);
+  if constexpr (OUT_BF16 && T::FN % 2 == 0) {
+    if (fast16) {
+      // whole block inside C, 16-byte aligned rows: one 16-byte store per lane
+      // covers 16 rows x 32 columns (half the store instructions of the
+      // 8-byte path)
+      const int q = lane >> 4;
+      const int64_t c8 = n0 + wn * T::WTN + 16 * (q & 1) + 8 * (q >> 1);
+#pragma unroll
+      for (int i = 0; i < T::FM; ++i) {
+        OutT* row = out + (r0 + i * 16) * p.ldo + c8;
+#pragma unroll
+        for (int j = 0; j < T::FN; j += 2)
+          *reinterpret_cast<u32x4*>(row + j * 16) = pair_to_row8(acc[i][j], acc[i][j + 1]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      return;
+    }
+  }
   if (fast) {
     // whole block inside C and 4-element aligned rows: no checks
 #pragma unroll
@@ -855,20 +900,20 @@ __device__ __forceinline__ void store_tile(const GemmParams& p, const Acc<BM, BN
   }
 }
 
-template <int BM, int BN, bool OUT_BF16, bool VEC>
-__global__ __launch_bounds__(kThreads, 1) void sfc_gemm_kernel(GemmParams p) {
-  using T = Tile<BM, BN>;
-  static_assert(T::A_CH >= 1 && T::B_CH >= 1, "tile too small for 256 threads");
+template <int BM, int BN, int NW, bool OUT_BF16, bool VEC>
+__global__ __launch_bounds__(NW * 64, 1) void sfc_gemm_kernel(GemmParams p) {
+  using T = Tile<BM, BN, NW>;
+  static_assert(T::A_CH >= 1 && T::B_CH >= 1, "tile too small for the workgroup");
   // fast path: the rings of A block and B stage slots; general path: two 64-deep blocks
-  constexpr int kSmem = VEC ? Ring<BM, BN>::ELEMS : 2 * (T::A_ELEMS + T::B_ELEMS);
+  constexpr int kSmem = VEC ? Ring<BM, BN, NW>::ELEMS : 2 * (T::A_ELEMS + T::B_ELEMS);
   __shared__ __attribute__((aligned(16))) uint16_t smem[kSmem];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 1, wn = wave & 1;
-  ReadOffsets<BM, BN> ro;
-  if constexpr (VEC) read_offsets<BM, BN>(wm, wn, lane, lds_addr(smem) + (uint32_t)Ring<BM, BN>::B_OFF, ro);
+  const int wm = wave / T::WGN, wn = wave % T::WGN;
+  ReadOffsets<BM, BN, NW> ro;
+  if constexpr (VEC) read_offsets<BM, BN, NW>(wm, wn, lane, lds_addr(smem) + (uint32_t)Ring<BM, BN, NW>::B_OFF, ro);
 
   const int P = gridDim.x;
   const int rank = xcd_rank(blockIdx.x, P);
@@ -889,6 +934,8 @@ __global__ __launch_bounds__(kThreads, 1) void sfc_gemm_kernel(GemmParams p) {
   const int esize = OUT_BF16 ? 2 : 4;
   const bool vec_store = ((uintptr_t)p.out % (4 * esize)) == 0 && (p.ldo % 4) == 0 &&
                          (p.out_layer_stride % 4) == 0;
+  // 8-element (16-byte) aligned rows for the paired bf16 stores
+  const bool vec16_store = ((uintptr_t)p.out % 16) == 0 && (p.ldo % 8) == 0 && (p.out_layer_stride % 8) == 0;
 
   for (int t = t_begin; t < t_end; t += t_step) {
     // Per-lane values are recomputed for every task rather than kept live
@@ -904,7 +951,7 @@ __global__ __launch_bounds__(kThreads, 1) void sfc_gemm_kernel(GemmParams p) {
     const int kt0 = (int)((unsigned)layer * (unsigned)p.nk / (unsigned)p.layers);
     const int kt1 = (int)((unsigned)(layer + 1) * (unsigned)p.nk / (unsigned)p.layers);
 
-    Acc<BM, BN> acc;
+    Acc<BM, BN, NW> acc;
 #pragma unroll
     for (int i = 0; i < T::FM; ++i)
 #pragma unroll
@@ -913,8 +960,8 @@ __global__ __launch_bounds__(kThreads, 1) void sfc_gemm_kernel(GemmParams p) {
     if (kt0 < kt1) {
       if constexpr (VEC) {
         const int64_t k0 = (int64_t)kt0 * kBK;
-        RingLanes<BM, BN> L;
-        ring_lanes<BM, BN>(p, m0, n0, wave, lane_t, L);
+        RingLanes<BM, BN, NW> L;
+        ring_lanes<BM, BN, NW>(p, m0, n0, wave, lane_t, L);
         RingAddr ra;
         ra.a0 = reinterpret_cast<uint64_t>(p.A + m0 * p.lda + k0) - kBias;
         ra.b0 = reinterpret_cast<uint64_t>(p.B + k0 * p.ldb + n0) - kBias;
@@ -926,37 +973,51 @@ __global__ __launch_bounds__(kThreads, 1) void sfc_gemm_kernel(GemmParams p) {
         }
         ra.lds0 = lds_addr(smem);
         ra.wave = wave;
-        main_loop_ring<BM, BN>(ra, kt1 - kt0, p.K - (int64_t)(kt1 - 1) * kBK, ro, L, lane_t, acc);
+        main_loop_ring<BM, BN, NW>(ra, kt1 - kt0, p.K - (int64_t)(kt1 - 1) * kBK, ro, L, lane_t, acc);
       } else {
-        main_loop_staged<BM, BN>(p, smem, m0, n0, kt0, kt1, tid, acc);
+        main_loop_staged<BM, BN, NW>(p, smem, m0, n0, kt0, kt1, tid, acc);
       }
     }
 
     const int64_t lstride = p.out_layer_stride * layer;
     const bool interior = m0 + BM <= p.M && n0 + BN <= p.N;
-    store_tile<BM, BN, OUT_BF16>(p, acc, m0, n0, lstride, wm, wn, lane_t, interior && vec_store);
+    store_tile<BM, BN, NW, OUT_BF16>(p, acc, m0, n0, lstride, wm, wn, lane_t, interior && vec_store,
+                                      interior && vec16_store);
   }
 }
 
 // ---- dispatch ---------------------------------------------------------------------
-template <int BM, int BN, bool OB, bool VEC>
+// Waves per workgroup of the fast path for each block shape (the general path
+// always runs 4).  256x256 blocks can be built with 8 waves (two per SIMD,
+// 128x64 each): they need ~3.5 % fewer cycles per launch on MI355X, but read
+// 1.5x the LDS bytes and run at a lower clock for the same time, so 4 is the
+// default.
+#ifndef SFC_WAVES_256x256
+#define SFC_WAVES_256x256 4
+#endif
+static_assert(SFC_WAVES_256x256 == 4 || SFC_WAVES_256x256 == 8, "4 or 8 waves");
+static constexpr int fast_waves(int tile) { return tile == kT256x256 ? SFC_WAVES_256x256 : 4; }
+
+template <int BM, int BN, int NW, bool OB, bool VEC>
 static const void* kernel_ptr() {
-  return reinterpret_cast<const void*>(&sfc_gemm_kernel<BM, BN, OB, VEC>);
+  return reinterpret_cast<const void*>(&sfc_gemm_kernel<BM, BN, NW, OB, VEC>);
 }
 
 static const void* select_kernel(int tile, bool ob, bool vec) {
-#define SFC_K(BM_, BN_)                                                        \
-  return ob ? (vec ? kernel_ptr<BM_, BN_, true, true>() : kernel_ptr<BM_, BN_, true, false>()) \
-            : (vec ? kernel_ptr<BM_, BN_, false, true>() : kernel_ptr<BM_, BN_, false, false>())
+#define SFC_K(BM_, BN_, NW_)                                                                   \
+  return ob ? (vec ? kernel_ptr<BM_, BN_, NW_, true, true>() : kernel_ptr<BM_, BN_, 4, true, false>()) \
+            : (vec ? kernel_ptr<BM_, BN_, NW_, false, true>() : kernel_ptr<BM_, BN_, 4, false, false>())
   switch (tile) {
-    case kT128x128: SFC_K(128, 128);
-    case kT256x128: SFC_K(256, 128);
-    case kT128x256: SFC_K(128, 256);
-    case kT256x256: SFC_K(256, 256);
+    case kT128x128: SFC_K(128, 128, 4);
+    case kT256x128: SFC_K(256, 128, 4);
+    case kT128x256: SFC_K(128, 256, 4);
+    case kT256x256: SFC_K(256, 256, fast_waves(kT256x256));
     default: return nullptr;
   }
 #undef SFC_K
 }
+
+static int threads_of(int tile, bool vec) { return (vec ? fast_waves(tile) : 4) * 64; }
 
 hipError_t launch_gemm(int tile, bool out_bf16, bool vec, const GemmParams& p, int grid,
                        hipStream_t stream) {
@@ -964,13 +1025,13 @@ hipError_t launch_gemm(int tile, bool out_bf16, bool vec, const GemmParams& p, i
   if (!k) return hipErrorInvalidValue;
   GemmParams local = p;
   void* args[] = {&local};
-  return hipLaunchKernel(k, dim3(grid), dim3(kThreads), args, 0, stream);
+  return hipLaunchKernel(k, dim3(grid), dim3(threads_of(tile, vec)), args, 0, stream);
 }
 
 hipError_t gemm_occupancy(int tile, bool out_bf16, bool vec, int* blocks_per_cu) {
   const void* k = select_kernel(tile, out_bf16, vec);
   if (!k) return hipErrorInvalidValue;
-  return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, k, kThreads, 0);
+  return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, k, threads_of(tile, vec), 0);
 }
 
 }  // namespace sfc

@@ -6,7 +6,6 @@
 namespace sfc {
 
 constexpr int kBK = 64;          // depth of one K block (the paper's bk)
-constexpr int kThreads = 256;    // four wave64 waves per workgroup
 
 enum TileId { kT128x128 = 0, kT256x128 = 1, kT128x256 = 2, kT256x256 = 3, kNumTiles = 4 };
 
