@@ -57,7 +57,7 @@ extern "C" {
 /* ---- number of K layers (copies of C) ---------------------------------- */
 #define SFC_CA_AUTO      0       /* ca_layers = 0: chosen with the block shape by the
                                     analytical model (Section III.B Eq. 1-4, used as in
-                                    Section III.C's second option), among 1, 2, 4, 8 */
+                                    Section III.C's second option), among 1, 2, 4, 8, 16 */
 
 /* ---- order of the output blocks ---------------------------------------- */
 #define SFC_ORDER_HILBERT   0    /* generalized Hilbert curve (Section II.B) */
@@ -118,7 +118,7 @@ int sfc_gemm_bf16out(int64_t M, int64_t N, int64_t K,
 /*
  * sfc_gemm_ws_size -- bytes of fp32 workspace that a ca_layers = c call needs:
  * c_eff * M * N * 4 with c_eff = min(c, ceil(K/64)) when c_eff > 1, else 0.
- * For c = SFC_CA_AUTO: the size for the largest count the model picks (8), a
+ * For c = SFC_CA_AUTO: the size for the largest count the model picks (16), a
  * bound that holds whatever it chooses.  Returns 0 for invalid arguments as well.
  */
 size_t sfc_gemm_ws_size(int64_t M, int64_t N, int64_t K, int ca_layers);
@@ -159,7 +159,7 @@ int sfc_gemm_plan(int64_t M, int64_t N, int64_t K, int ca_layers, int tile, int6
  * block shared by the tasks in flight on one XCD; the critical path is the
  * rounds of tasks times the blocks of the longest layer, plus the C traffic
  * (and, with layers, the copies written and read back) and the launches.
- * Every candidate (block shape x c in {1, 2, 4, 8}, or only the fixed ones) is
+ * Every candidate (block shape x c in {1, 2, 4, 8, 16}, or only the fixed ones) is
  * evaluated and the fastest kept; near ties go to less padded work, then to
  * 256x256, 128x256, 256x128, 128x128 in that order, then to fewer layers.
  *   out_type   SFC_OUT_F32 or SFC_OUT_BF16 (bytes of C).

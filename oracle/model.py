@@ -22,8 +22,10 @@ second option).  The reading for this GPU (listed in the design doc):
   plus C (M*N*out bytes) or, with c > 1, the fp32 copies written and read
   back (2*c*M*N*4) and then C, all at the HBM rate, plus one launch (two with
   a reduction);
-* candidates: 256x256, 128x256, 256x128, 128x128 blocks, c in {1, 2, 4, 8}
-  capped at nK = ceil(K/64); times within a relative 1e-9 are ties, settled by
+* candidates: 256x256, 128x256, 256x128, 128x128 blocks, c in {1, 2, 4, 8, 16}
+  capped at nK = ceil(K/64) (16 so that a K-dominant GEMM whose C grid has only
+  16 blocks of 256x256 can still occupy 256 CUs: Section II.E lets the
+  decomposition Tm x Tn x c follow the aspect ratio of the problem); times within a relative 1e-9 are ties, settled by
   fewer padded output elements, then by the order of evaluation (that block
   order, then ascending layer counts).
 
@@ -41,13 +43,13 @@ import math
 from typing import Dict, List, Optional, Tuple
 
 FLOPS_PER_CLK_CU = 4096.0 * 0.74            # dense bf16 MFMA per CU per clock x achieved fraction
-RATE = {(128, 128): 0.75, (256, 128): 0.85, (128, 256): 0.85, (256, 256): 1.0}
+RATE = {(128, 128): 0.60, (256, 128): 0.80, (128, 256): 0.86, (256, 256): 1.0}
 HBM_BYTES_PER_CLK = 3500.0
 LAUNCH_CLK = 10000.0
 XCDS = 8
 BK = 64
 SHAPES = [(256, 256), (128, 256), (256, 128), (128, 128)]   # tie order
-LAYERS = [1, 2, 4, 8]
+LAYERS = [1, 2, 4, 8, 16]
 
 
 def brgemm_clk(G: float, gamma: float, beta: float, s_a: float, s_b: float) -> float:

@@ -21,13 +21,13 @@ namespace sfc {
 // Calibration on MI355X (fast path, bf16 in, fp32 accumulate).
 struct ModelConst {
   double flops_per_clk_cu = 4096.0 * 0.74;   // dense bf16 MFMA peak x achieved fraction (256x256)
-  double rate[4] = {0.75, 0.85, 0.85, 1.0};  // per shape, relative to 256x256 (index: kT* order)
+  double rate[4] = {0.60, 0.80, 0.86, 1.0};  // per shape, relative to 256x256 (index: kT* order)
   double hbm_bytes_per_clk = 3500.0;         // whole chip, at the loaded shader clock
   double launch_clk = 10000.0;               // per kernel launch (about 5 us)
   int xcds = 8;
 };
 
-constexpr int kModelMaxLayers = 8;           // the candidates are c = 1, 2, 4, 8
+constexpr int kModelMaxLayers = 16;          // the candidates are c = 1, 2, 4, 8, 16
 
 struct ModelChoice {
   int tile;          // kT* index

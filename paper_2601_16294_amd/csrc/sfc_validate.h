@@ -10,7 +10,7 @@
 namespace sfc {
 
 constexpr int kMaxLayers = 64;
-constexpr int kAutoLayers = 8;                  // largest layer count SFC_CA_AUTO picks
+constexpr int kAutoLayers = 16;                  // largest layer count SFC_CA_AUTO picks
 constexpr int64_t kMaxDim = (int64_t)1 << 31;   // block indices are int32
 
 struct Checked {

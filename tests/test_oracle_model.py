@@ -30,18 +30,21 @@ def test_eq1_memory_bound_block():
 def test_worked_estimate_kdominant_128x256_c8():
     # 1024 x 1024 x 65536, fp32 out, 128x256 blocks, 8 layers, 256 CUs, 1 per CU:
     # 8*4*8 = 256 tasks in 1 round; 1024 K blocks / 8 = 128 blocks per task;
-    # block: 4,194,304 flops / (3031.04 * 0.85) = 1627.98 clk (compute-bound:
+    # block: 4,194,304 flops / (3031.04 * 0.86) = 1609.0509 clk (compute-bound:
     # panels 49,152 B * 256/3500 / sqrt(32) = 635.53 clk);
     # copies 2*8*1024*1024*4 + C 1024*1024*4 = 71,303,168 B / 3500 = 20,372.3 clk;
-    # 2 launches = 20,000 clk.  Total 248,753.89 clk.
+    # 2 launches = 20,000 clk.  Total 246,330.85 clk.
     occ = {(128, 128): 2, (256, 128): 1, (128, 256): 1, (256, 256): 1}
     clk, pad = om.estimate(1024, 1024, 65536, 4, 256, occ, (128, 256), 8)
-    assert clk == pytest.approx(248753.89, rel=1e-8)
+    assert clk == pytest.approx(246330.85, rel=1e-8)
     assert pad == 256 * 128 * 256
 
 
 @pytest.mark.parametrize("M,N,K", [(3000, 7000, 2048), (1024, 4096, 8192), (8192, 512, 65536), (777, 5000, 1000)])
-def test_model_is_symmetric_in_m_and_n(M, N, K):
+def test_model_is_symmetric_in_m_and_n(M, N, K, monkeypatch):
+    # the formula treats M and N alike; the calibrated rates of 128x256 and
+    # 256x128 differ (two kernels), so the check runs with equal rates
+    monkeypatch.setattr(om, "RATE", {**om.RATE, (256, 128): om.RATE[(128, 256)]})
     occ = {(128, 128): 2, (256, 128): 1, (128, 256): 1, (256, 256): 1}
     for (bm, bn) in om.SHAPES:
         for c in om.LAYERS:
@@ -81,7 +84,7 @@ def test_ties_keep_the_first_candidate():
 def test_worked_estimate_memory_bound():
     # 8192^3, fp32 out, 128x256 blocks, 1 layer, on a device of 4096 CUs:
     # 64*32 = 2048 tasks, all in flight (1 round), 256 per XCD (sqrt = 16);
-    # block: panels 49,152 B * 2048/3500 / 16 = 1797.56 clk > compute 1627.98;
+    # block: panels 49,152 B * 2048/3500 / 16 = 1797.56 clk > compute 1609.05;
     # 128 blocks; C 8192*8192*4 B / 3500 = 76,695.4 clk; 1 launch.
     # Total 316,783.38 clk.
     occ = {(128, 128): 2, (256, 128): 1, (128, 256): 1, (256, 256): 1}
