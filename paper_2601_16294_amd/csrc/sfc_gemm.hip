@@ -139,15 +139,21 @@ __device__ __forceinline__ void wait_lds_all() { asm volatile("s_waitcnt lgkmcnt
 // The MFMA takes the B fragment as its first operand, so it computes the
 // transposed 16x16 block: lane l ends with row l%16 of the fragment and its 4
 // consecutive columns 4*(l/16) .. +3.
-// NW waves per workgroup in a 2 x (NW/2) grid: 4 waves (one per SIMD) or 8
+// NW waves per workgroup in a WGM x WGN grid: 4 waves (one per SIMD) or 8
 // (two per SIMD, so that one wave's MFMAs run while the other issues its reads,
-// loads and waits).
+// loads and waits).  A wave's fragment reads per 32-deep step are FM b128
+// reads of A and 2*FN transposing reads of B, so the grid keeps the wave
+// sub-block at most twice as wide as tall.
 template <int BM, int BN, int NW>
 struct Tile {
   static_assert(NW == 4 || NW == 8, "4 or 8 waves");
   static constexpr int THREADS = NW * 64;
-  static constexpr int WGN = NW / 2;                  // waves along N
-  static constexpr int WTM = BM / 2, WTN = BN / WGN;  // wave sub-block
+#ifndef SFC_WGM_128x256
+#define SFC_WGM_128x256 1
+#endif
+  static constexpr int WGM = (NW == 4 && BM == 128 && BN == 256) ? SFC_WGM_128x256 : 2;  // waves along M
+  static constexpr int WGN = NW / WGM;                // waves along N
+  static constexpr int WTM = BM / WGM, WTN = BN / WGN;  // wave sub-block
   static constexpr int FM = WTM / 16, FN = WTN / 16;  // 16x16 fragments per wave
   static constexpr int A_ELEMS = BM * kBK, B_ELEMS = kBK * BN;
   static constexpr int A_CH = BM * kBK / 8 / THREADS;   // 16-byte chunks per thread

@@ -228,3 +228,28 @@ def test_auto_layers_match_oracle(M, N, K, out):
     model = sg().sfc_gemm_model(M, N, K, out="f32", ca_layers=0, num_cus=cus, occupancy=occ)
     assert (f"{plan['BM']}x{plan['BN']}", plan["layers"]) == (model["tile"], model["layers"])
     assert plan["layers"] > 1
+
+
+@pytest.mark.parametrize("tile", TILES)
+def test_bf16_store_paths_by_alignment(tile):
+    """The bf16 epilogue has three store paths: 16-byte stores of paired
+    fragments (C 16-byte aligned, ldc a multiple of 8), 8-byte stores (8-byte
+    aligned, ldc a multiple of 4) and element stores (anything else).  Each must
+    give the RNE of the fp32 result bit for bit and leave the padding alone."""
+    M, N, K = 300, 520, 200
+    A, B = operands(M, N, K, 1200, dist=("normal", 0, 1))
+    dA, dB = upload(A), upload(B)
+    C32 = torch.empty((M, N), dtype=torch.float32, device="cuda")
+    sg().sfc_gemm_ex(dA, dB, C32, tile=tile)
+    torch.cuda.synchronize()
+    want = obf16.f32_to_bf16_rne(C32.cpu().numpy())
+    for offset, ldc in ((0, 520), (4, 524), (1, 523)):
+        buf = torch.full((offset + M * ldc,), float("nan"), dtype=torch.bfloat16, device="cuda")
+        C = buf[offset:].view(M, ldc)[:, :N]
+        sg().sfc_gemm_ex(dA, dB, C, tile=tile)
+        torch.cuda.synchronize()
+        full = raw_bits(buf[offset:].view(M, ldc))
+        assert np.array_equal(full[:, :N], want), (tile, offset, ldc)
+        pad = to_host(buf[offset:].view(M, ldc))[:, N:]
+        assert np.isnan(pad).all(), (tile, offset, ldc)
+        assert np.isnan(to_host(buf[:offset])).all()
