@@ -13,7 +13,12 @@ line also carries:
   * cpu_baseline -- the CPU oracle on a bounded row sample of the same GEMM;
   * workloads  -- every measured workload (TFLOP/s, cold and warm, the paper's
                   protocol of 10 cold repetitions) and their flop-weighted
-                  harmonic mean.
+                  harmonic mean;
+  * sweep      -- with --sweep: the paper's 125-shape cube sweep (Section IV.A),
+                  per shape the library's own choice of block shape and layer
+                  count (10 cold repetitions), the best of a small autotune
+                  over the layer count, the fraction of the shape's roofline,
+                  and the flop-weighted harmonic mean.
 Inputs are synthetic (seeded, see paper_2601_16294_amd/inputs.py).
 """
 from __future__ import annotations
@@ -51,6 +56,8 @@ def parse():
     ap.add_argument("--order", default="hilbert", choices=["hilbert", "row_major"])
     ap.add_argument("--sched", default="interleaved", choices=["interleaved", "block"])
     ap.add_argument("--only", default=None, help="run the kernel of one workload K times and exit")
+    ap.add_argument("--sweep", action="store_true", help="also run the 125-shape sweep")
+    ap.add_argument("--sweep-reps", type=int, default=3, help="cold repetitions per autotune candidate")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="with --only: also run a plain device copy of MIB MiB (counter calibration)")
     return ap.parse_args()
@@ -67,6 +74,80 @@ def traffic_record():
     if rec.get("kernel_src_sha256") != sha:
         return None
     return rec.get("hbm_bytes_per_launch")
+
+
+def roofline_tflops(M, N, K, out_bytes):
+    """min(MFMA peak, OI x HBM bandwidth) with compulsory bytes A + B + C."""
+    oi = 2.0 * M * N * K / (2.0 * M * K + 2.0 * K * N + out_bytes * M * N)
+    hbm = oi * PEAK_HBM_GBS / 1e3
+    return ("hbm", hbm) if hbm < PEAK_BF16_TFLOPS else ("mfma", PEAK_BF16_TFLOPS)
+
+
+def run_sweep(args, sg, torch, stream, dev):
+    """The 125-shape sweep: the library's choice (SFC_TILE_AUTO, SFC_CA_AUTO),
+    timed cold (10 repetitions, 512 MiB flush between), and an autotune over
+    ca_layers in {1, 2, 4, 8, 16} with the model's block shape for each count."""
+    from paper_2601_16294_amd.inputs import draw, sweep_gemms
+    flush = torch.empty(512 * 1024 * 1024 // 4, dtype=torch.float32, device=dev)
+    cus = torch.cuda.get_device_properties(dev).multi_processor_count
+    occ = tuple(sg.sfc_gemm_plan(8192, 8192, 64, 1, t)["per_cu"] for t in ("128x128", "256x128", "128x256", "256x256"))
+    mats = {}
+
+    def mat(rows, cols, dist, seed):
+        if seed not in mats:
+            mats[seed] = sg.to_device_bf16(draw(rows, cols, dist, seed))
+        return mats[seed]
+
+    def cold(a, b, c, layers, tile, reps):
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+        for s0, s1 in ev:
+            flush.zero_()
+            s0.record(stream)
+            sg.sfc_gemm_ex(a, b, c, ca_layers=layers, tile=tile, stream=stream)
+            s1.record(stream)
+        torch.cuda.synchronize()
+        return sum(x.elapsed_time(y) for x, y in ev) / reps
+
+    rows = []
+    num = den = 0.0
+    for g in sweep_gemms():
+        a = mat(g.M, g.K, g.dist_a, g.seed_a)
+        b = mat(g.K, g.N, g.dist_b, g.seed_b)
+        c = torch.empty((g.M, g.N), dtype=torch.bfloat16, device=dev)
+        choice = sg.sfc_gemm_model(g.M, g.N, g.K, out="bf16", num_cus=cus, occupancy=occ)
+        for _ in range(2):
+            sg.sfc_gemm_ex(a, b, c, ca_layers=0, tile="auto", stream=stream)
+        ms = cold(a, b, c, 0, "auto", args.reps)
+        tuned = []
+        for layers in (1, 2, 4, 8, 16):
+            t = sg.sfc_gemm_model(g.M, g.N, g.K, out="bf16", ca_layers=layers, num_cus=cus, occupancy=occ)["tile"]
+            sg.sfc_gemm_ex(a, b, c, ca_layers=layers, tile=t, stream=stream)
+            tuned.append((cold(a, b, c, layers, t, args.sweep_reps), t, layers))
+        best = min(tuned)
+        bound, roof = roofline_tflops(g.M, g.N, g.K, 2)
+        tf = g.flops / (ms * 1e-3) / 1e12
+        rows.append({"M": g.M, "N": g.N, "K": g.K, "tile": choice["tile"], "ca_layers": choice["layers"],
+                     "ms": round(ms, 4), "tflops": round(tf, 1), "bound": bound,
+                     "frac_roofline": round(tf / roof, 4),
+                     "best": {"tile": best[1], "ca_layers": best[2], "ms": round(best[0], 4),
+                              "tflops": round(g.flops / (best[0] * 1e-3) / 1e12, 1)}})
+        num += g.flops
+        den += g.flops / tf
+        log(f"[sweep] {g.M}x{g.N}x{g.K} {choice} {tf:.1f} TFLOP/s, best {rows[-1]['best']}")
+        del c
+    del flush, mats
+    torch.cuda.empty_cache()
+    best_num = sum(2.0 * r["M"] * r["N"] * r["K"] for r in rows)
+    best_den = sum(2.0 * r["M"] * r["N"] * r["K"] / r["best"]["tflops"] for r in rows)
+    ratio = [r["tflops"] / r["best"]["tflops"] for r in rows]
+    return {"protocol": f"bf16 in, fp32 accumulate, bf16 out, U(-1,1); mean of {args.reps} cold reps "
+                        f"(512 MiB flush between) of the library's choice; autotune: ca_layers in "
+                        f"{{1,2,4,8,16}} with the model's block shape, {args.sweep_reps} cold reps each",
+            "whm_tflops": round(num / den, 2), "whm_tflops_autotuned": round(best_num / best_den, 2),
+            "model_over_autotune_mean": round(sum(ratio) / len(ratio), 4),
+            "model_over_autotune_min": round(min(ratio), 4),
+            "worst_frac_roofline": min(r["frac_roofline"] for r in rows),
+            "shapes": rows}
 
 
 def main():
@@ -232,6 +313,8 @@ def main():
                  "shapes": table, "whm_tflops": round(whm, 2),
                  "whm_over_best_shape": round(whm / best_shape, 4)}
 
+    sweep = run_sweep(args, sg, torch, stream, dev) if args.sweep else None
+
     # ------------------------------------------------------------ cpu baseline
     cpu = None
     if not args.no_cpu_baseline:
@@ -270,6 +353,8 @@ def main():
         "library_same_workload": library,
         "workloads": table,
     }
+    if sweep is not None:
+        line["sweep"] = sweep
     print(json.dumps(line), flush=True)
 
 

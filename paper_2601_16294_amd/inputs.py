@@ -10,7 +10,7 @@ dimension.  Padding columns (ld > cols) hold a NaN sentinel so that a kernel
 that reads them shows it.
 
 Workloads (the paper's shapes and roles: Section IV.A's cube sweep, the
-Llama-3-8B prefill projections of Section IV.C) are synthetic stand-ins; no
+Llama-3-8B prefill projections of Section IV.D) are synthetic stand-ins; no
 dataset or trained weight is involved.
 """
 from __future__ import annotations
@@ -105,6 +105,25 @@ def workloads() -> List[Workload]:
                        5000 + 10 * j + 1, 5000 + 10 * j + 2, out="bf16")
                   for j, (n, k) in enumerate([(4096, 4096), (14336, 4096), (4096, 14336)])]),
     ]
+
+
+SWEEP_DIMS = (512, 1024, 2048, 4096, 8192)
+
+
+def sweep_gemms() -> List[Gemm]:
+    """The 125-shape sweep of Section IV.A: M, N, K each from {512, 1024, 2048,
+    4096, 8192}, bf16 inputs U(-1, 1), bf16 output.  A depends only on (M, K)
+    and B only on (K, N), so 25 A matrices and 25 B matrices serve every shape:
+    A of (M, K) = (d_i, d_k) uses seed 700000 + 100i + 10k + 1, B of (K, N) =
+    (d_k, d_n) uses 700000 + 100k + 10n + 2."""
+    U = ("uniform", -1.0, 1.0)
+    out = []
+    for i, M in enumerate(SWEEP_DIMS):
+        for j, N in enumerate(SWEEP_DIMS):
+            for k, K in enumerate(SWEEP_DIMS):
+                out.append(Gemm(M, N, K, U, U, 700000 + 100 * i + 10 * k + 1, 700000 + 100 * k + 10 * j + 2,
+                                out="bf16"))
+    return out
 
 
 def workload(name: str) -> Workload:
