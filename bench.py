@@ -14,6 +14,9 @@ line also carries:
   * workloads  -- every measured workload (TFLOP/s, cold and warm, the paper's
                   protocol of 10 cold repetitions) and their flop-weighted
                   harmonic mean;
+  * fp8_square8192 -- the same 8192^3 GEMM with OCP FP8 E4M3 operands
+                  (sfc_gemm_f8_ex, bf16 output), timed like the headline,
+                  against the fp8 dense MFMA peak;
   * sweep      -- with --sweep: the paper's 125-shape cube sweep (Section IV.A),
                   per shape the library's own choice of block shape and layer
                   count (10 cold repetitions), the best of a small autotune
@@ -35,6 +38,8 @@ METRIC = "bf16 GEMM TFLOP/s per shape + weighted harmonic mean; % of MFMA peak"
 # MI355X bf16 dense MFMA peak: 256 CUs x 4096 FLOP/clock x 2.4 GHz.
 PEAK_BF16_TFLOPS = 2516.6
 PEAK_HBM_GBS = 8000.0
+# MI355X fp8 dense MFMA peak (the published 5.0 PFLOP/s): twice the bf16 rate.
+PEAK_FP8_TFLOPS = 5033.2
 HEADLINE = "square8192_bf16out_t256"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_square8192_gemm.json")
 GEMM_SRC = os.path.join(ROOT, "paper_2601_16294_amd", "csrc", "sfc_gemm.hip")
@@ -243,6 +248,29 @@ def main():
     del dA, dB, C, ref
     torch.cuda.empty_cache()
 
+    # ------------------------------------------------- fp8 operands, same shape
+    from paper_2601_16294_amd.inputs import draw_e4m3
+    log("[bench] fp8 operands")
+    a8 = sg.to_device_u8(draw_e4m3(g.M, g.K, ("normal", 0.0, 1.0), 2101))
+    b8 = sg.to_device_u8(draw_e4m3(g.K, g.N, ("normal", 0.0, 1.0), 2102))
+    c8 = torch.empty((g.M, g.N), dtype=torch.bfloat16, device=dev)
+    for _ in range(args.warmup):
+        sg.sfc_gemm_f8_ex(a8, b8, c8, stream=stream)
+    torch.cuda.synchronize()
+    ev8 = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    for s0, s1 in ev8:
+        s0.record(stream)
+        sg.sfc_gemm_f8_ex(a8, b8, c8, stream=stream)
+        s1.record(stream)
+    torch.cuda.synchronize()
+    f8_ms = sum(x.elapsed_time(y) for x, y in ev8) / args.steps
+    f8_tf = g.flops / (f8_ms * 1e-3) / 1e12
+    fp8 = {"call": "sfc_gemm_f8_ex, E4M3 A and B ~ N(0,1), bf16 out, 256x256 blocks", "ms": round(f8_ms, 4),
+           "tflops": round(f8_tf, 1), "peak": PEAK_FP8_TFLOPS, "frac": round(f8_tf / PEAK_FP8_TFLOPS, 4)}
+    log(f"[bench] fp8 {fp8}")
+    del a8, b8, c8
+    torch.cuda.empty_cache()
+
     # ---------------------------------------------- sustained MFMA throughput
     # Register-only MFMA loops: the clock the chip holds depends on how much the
     # operand bits toggle, so the achievable ceiling for random data sits well
@@ -351,6 +379,7 @@ def main():
                      "frac_of_probe_random": round(achieved / probe["random_operands"]["tflops"], 4)},
         "cpu_baseline": cpu,
         "library_same_workload": library,
+        "fp8_square8192": fp8,
         "workloads": table,
     }
     if sweep is not None:

@@ -141,6 +141,28 @@ int sfc_gemm_ex(int64_t M, int64_t N, int64_t K,
                 void *ws, size_t ws_bytes, void *stream);
 
 /*
+ * sfc_gemm_f8_ex -- C = A * B with 8-bit float operands (the paper leaves the
+ * data type a parameter of the method, Section III.A): A and B hold OCP FP8
+ * E4M3 bytes (1 sign, 4 exponent bits with bias 7, 3 mantissa bits; no
+ * infinities, 0x7F / 0xFF are NaN), row-major, lda and ldb in elements (=
+ * bytes).  The products are exact in fp32 and the sums are fp32, as in
+ * sfc_gemm_ex; C is fp32 or bf16 (out_type).  Same blocks-along-the-curve and
+ * K-layer scheme, with K blocks 128 deep: ca_layers = c uses min(c,
+ * ceil(K/128)) layers, whose workspace sfc_gemm_ws_size(M, N, K, c) bounds.
+ * Restrictions (else SFC_ERR_UNSUPPORTED, nothing enqueued): A and B 16-byte
+ * aligned, lda, ldb, K and N multiples of 16; tile SFC_TILE_AUTO or
+ * SFC_TILE_256x256 (256x256 blocks); ca_layers >= 1 (SFC_CA_AUTO is not
+ * offered: the model is calibrated for bf16).  Other arguments and errors as
+ * for sfc_gemm_ex.
+ */
+int sfc_gemm_f8_ex(int64_t M, int64_t N, int64_t K,
+                   const void *A, int64_t lda,
+                   const void *B, int64_t ldb,
+                   void *C, int64_t ldc,
+                   int out_type, int ca_layers, int tile, int order, int sched,
+                   void *ws, size_t ws_bytes, void *stream);
+
+/*
  * sfc_gemm_plan -- what sfc_gemm_ex would launch, without launching
  * (fp32 output, 16-byte aligned operands).  ca_layers may be SFC_CA_AUTO and
  * tile SFC_TILE_AUTO; the plan then shows the model's choice.

@@ -51,6 +51,9 @@ typedef short i16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef int i32x8 __attribute__((ext_vector_type(8)));
+typedef int i32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 typedef __attribute__((address_space(3))) const bf16x8 lds_bf16x8;
@@ -144,7 +147,7 @@ __device__ __forceinline__ void wait_lds_all() { asm volatile("s_waitcnt lgkmcnt
 // loads and waits).  A wave's fragment reads per 32-deep step are FM b128
 // reads of A and 2*FN transposing reads of B, so the grid keeps the wave
 // sub-block at most twice as wide as tall.
-template <int BM, int BN, int NW>
+template <int BM, int BN, int NW, bool F8>
 struct Tile {
   static_assert(NW == 4 || NW == 8, "4 or 8 waves");
   static constexpr int THREADS = NW * 64;
@@ -154,19 +157,28 @@ struct Tile {
   static constexpr int WGM = (NW == 4 && BM == 128 && BN == 256) ? SFC_WGM_128x256 : 2;  // waves along M
   static constexpr int WGN = NW / WGM;                // waves along N
   static constexpr int WTM = BM / WGM, WTN = BN / WGN;  // wave sub-block
-  static constexpr int FM = WTM / 16, FN = WTN / 16;  // 16x16 fragments per wave
+  // fragments per wave: 16x16 (bf16, MFMA 16x16x32) or 32x32 (fp8, MFMA 32x32x64)
+  static constexpr int FS = F8 ? 32 : 16;
+  static constexpr int FM = WTM / FS, FN = WTN / FS;
   static constexpr int A_ELEMS = BM * kBK, B_ELEMS = kBK * BN;
   static constexpr int A_CH = BM * kBK / 8 / THREADS;   // 16-byte chunks per thread
   static constexpr int B_CH = kBK * BN / 8 / THREADS;
 };
 
-template <int BM, int BN, int NW>
-using Acc = f32x4[Tile<BM, BN, NW>::FM][Tile<BM, BN, NW>::FN];
+// One accumulator fragment: 16x16 fp32 (4 per lane) or 32x32 fp32 (16 per lane).
+template <bool F8>
+using AccFrag = typename std::conditional<F8, f32x16, f32x4>::type;
+template <int BM, int BN, int NW, bool F8>
+using Acc = AccFrag<F8>[Tile<BM, BN, NW, F8>::FM][Tile<BM, BN, NW, F8>::FN];
 
-template <int BM, int BN, int NW>
+// Operand fragments of one step: 8 bf16 per lane (16x32), or 32 fp8 bytes per
+// lane (32x64).
+template <bool F8>
+using OpFrag = typename std::conditional<F8, i32x8, bf16x8>::type;
+template <int BM, int BN, int NW, bool F8>
 struct Frags {
-  bf16x8 a[Tile<BM, BN, NW>::FM];
-  bf16x8 b[Tile<BM, BN, NW>::FN];
+  OpFrag<F8> a[Tile<BM, BN, NW, F8>::FM];
+  OpFrag<F8> b[Tile<BM, BN, NW, F8>::FN];
 };
 
 // Per-lane LDS element offsets of the fragment reads of one 32-deep step:
@@ -199,10 +211,10 @@ __device__ __forceinline__ bf16x8 read_b_pair(const uint16_t* p, int half_stride
 
 // All operand fragments of one 32-deep step from an A block [BM][64] (step
 // ks) and a B buffer [..][BN] (rows kbase .. kbase+31).
-template <int BM, int BN, int NW>
+template <int BM, int BN, int NW, bool F8>
 __device__ __forceinline__ void load_frags(const uint16_t* As, const uint16_t* Bs, int wm, int wn,
-                                           int lane, int ks, int kbase, Frags<BM, BN, NW>& f) {
-  using T = Tile<BM, BN, NW>;
+                                           int lane, int ks, int kbase, Frags<BM, BN, NW, F8>& f) {
+  using T = Tile<BM, BN, NW, F8>;
   const int ao = a_frag_off(wm * T::WTM, lane, ks);
 #pragma unroll
   for (int i = 0; i < T::FM; ++i) f.a[i] = *reinterpret_cast<const bf16x8*>(As + ao + i * 16 * kBK);
@@ -211,9 +223,9 @@ __device__ __forceinline__ void load_frags(const uint16_t* As, const uint16_t* B
 }
 
 // acc += one 32-deep step.
-template <int BM, int BN, int NW>
-__device__ __forceinline__ void mma_step(const Frags<BM, BN, NW>& cur, Acc<BM, BN, NW>& acc) {
-  using T = Tile<BM, BN, NW>;
+template <int BM, int BN, int NW, bool F8>
+__device__ __forceinline__ void mma_step(const Frags<BM, BN, NW, F8>& cur, Acc<BM, BN, NW, F8>& acc) {
+  using T = Tile<BM, BN, NW, F8>;
 #pragma unroll
   for (int i = 0; i < T::FM; ++i)
 #pragma unroll
@@ -239,10 +251,23 @@ __device__ __forceinline__ void mma_step(const Frags<BM, BN, NW>& cur, Acc<BM, B
 constexpr int kSK = 32;        // K depth of one B stage (one MFMA step)
 constexpr int kBias = 4096;    // bytes; keeps every biased voffset positive
 
+// The rings hold the same bytes for both element types: a block row is 128
+// bytes (64 bf16 or 128 fp8 elements of K), a B stage is 64*BN bytes (32 rows
+// of BN bf16 or 64 rows of BN fp8).  K depth, in elements, of a block and of a
+// B stage:
+template <bool F8>
+constexpr int block_k() { return F8 ? 128 : kBK; }
+template <bool F8>
+constexpr int stage_k() { return F8 ? 64 : kSK; }
+// fp8 B stages: chunk c (16 columns) of row k is stored at chunk c ^ (2*(k&7));
+// a transposing read of 8 consecutive rows at two adjacent chunks (2m, 2m+1)
+// then touches 16 distinct 16-byte bank groups.
+__device__ __forceinline__ int b_swz8(int k) { return (k & 7) << 1; }
+
 // The loads of block b+D are issued during block b (prefetch depth D): the A
 // ring has D+1 block slots, the B ring 2D stage slots.  D = 3 where the LDS
 // holds that at the same occupancy (128x256: exactly 160 KiB), else 2.
-template <int BM, int BN, int NW>
+template <int BM, int BN, int NW, bool F8>
 struct Ring {
   static constexpr int A_BLK = BM * kBK;                 // elements of one A block
   static constexpr int B_STG = kSK * BN;                 // elements of one B stage
@@ -288,81 +313,149 @@ __device__ __forceinline__ i32x4 make_rsrc_addr(uint64_t a, uint32_t num_records
 }
 
 // Per-lane, per-task load offsets (bytes, biased).
-template <int BM, int BN, int NW>
+template <int BM, int BN, int NW, bool F8>
 struct RingLanes {
-  int a_voff[Ring<BM, BN, NW>::APB];
-  int b_voff[Ring<BM, BN, NW>::BPW];
+  int a_voff[Ring<BM, BN, NW, F8>::APB];
+  int b_voff[Ring<BM, BN, NW, F8>::BPW];
 };
 
-// K index (within a block) at which A load j of this lane starts.
+// K index (within a block, in elements) at which A load j of this lane starts.
+template <bool F8>
 __device__ __forceinline__ int a_load_k(int wave, int apb, int j, int lane) {
   const int row = (wave * apb + j) * 8 + (lane >> 3);
-  return ((lane & 7) ^ ((row >> 1) & 7)) * 8;
+  return ((lane & 7) ^ ((row >> 1) & 7)) * (F8 ? 16 : 8);
 }
 
-template <int BM, int BN, int NW>
+template <int BM, int BN, int NW, bool F8>
 __device__ __forceinline__ void ring_lanes(const GemmParams& p, int64_t m0, int64_t n0, int wave,
-                                           int lane, RingLanes<BM, BN, NW>& L) {
-  using R = Ring<BM, BN, NW>;
+                                           int lane, RingLanes<BM, BN, NW, F8>& L) {
+  using R = Ring<BM, BN, NW, F8>;
 #pragma unroll
   for (int j = 0; j < R::APB; ++j) {
     const int row = (wave * R::APB + j) * 8 + (lane >> 3);
     const int c = (lane & 7) ^ ((row >> 1) & 7);
-    L.a_voff[j] = (m0 + row < p.M) ? (int)((row * p.lda + c * 8) * 2) + kBias - (j & 3) * 1024 : kOobOffset;
+    if constexpr (F8)
+      L.a_voff[j] = (m0 + row < p.M) ? (int)(row * p.lda + c * 16) + kBias - (j & 3) * 1024 : kOobOffset;
+    else
+      L.a_voff[j] = (m0 + row < p.M) ? (int)((row * p.lda + c * 8) * 2) + kBias - (j & 3) * 1024 : kOobOffset;
   }
 #pragma unroll
   for (int j = 0; j < R::BPW; ++j) {
-    const int e = (wave * R::BPW + j) * 512 + lane * 8;   // element index in the [32][BN] stage
-    const int k = e / BN;
-    const int c = ((e % BN) >> 3) ^ b_swz(k);
-    L.b_voff[j] = (n0 + c * 8 < p.N) ? (int)((k * p.ldb + c * 8) * 2) + kBias - j * 1024 : kOobOffset;
+    if constexpr (F8) {
+      const int eb = (wave * R::BPW + j) * 1024 + lane * 16;   // byte offset in the [64][BN] stage
+      const int k = eb / BN;
+      const int c = ((eb % BN) >> 4) ^ b_swz8(k);
+      L.b_voff[j] = (n0 + c * 16 < p.N) ? (int)(k * p.ldb + c * 16) + kBias - j * 1024 : kOobOffset;
+    } else {
+      const int e = (wave * R::BPW + j) * 512 + lane * 8;   // element index in the [32][BN] stage
+      const int k = e / BN;
+      const int c = ((e % BN) >> 3) ^ b_swz(k);
+      L.b_voff[j] = (n0 + c * 8 < p.N) ? (int)((k * p.ldb + c * 8) * 2) + kBias - j * 1024 : kOobOffset;
+    }
   }
 }
 
 // Turn the A lanes whose load starts at a K index >= kin (within the block)
 // into out-of-range lanes, for the loads of a block that runs past K.
-template <int BM, int BN, int NW>
-__device__ __forceinline__ void mask_a_lanes(RingLanes<BM, BN, NW>& L, int wave, int lane, int64_t kin) {
-  using R = Ring<BM, BN, NW>;
+template <int BM, int BN, int NW, bool F8>
+__device__ __forceinline__ void mask_a_lanes(RingLanes<BM, BN, NW, F8>& L, int wave, int lane, int64_t kin) {
+  using R = Ring<BM, BN, NW, F8>;
 #pragma unroll
   for (int j = 0; j < R::APB; ++j)
-    if (a_load_k(wave, R::APB, j, lane) >= kin) L.a_voff[j] = kOobOffset;
+    if (a_load_k<F8>(wave, R::APB, j, lane) >= kin) L.a_voff[j] = kOobOffset;
 }
 
 // The same without a branch: masks only when `on` (wave-uniform).
-template <int BM, int BN, int NW>
-__device__ __forceinline__ void mask_a_lanes_if(RingLanes<BM, BN, NW>& L, int wave, int lane, int64_t kin, bool on) {
-  using R = Ring<BM, BN, NW>;
+template <int BM, int BN, int NW, bool F8>
+__device__ __forceinline__ void mask_a_lanes_if(RingLanes<BM, BN, NW, F8>& L, int wave, int lane, int64_t kin, bool on) {
+  using R = Ring<BM, BN, NW, F8>;
 #pragma unroll
   for (int j = 0; j < R::APB; ++j)
-    L.a_voff[j] = (on && a_load_k(wave, R::APB, j, lane) >= kin) ? kOobOffset : L.a_voff[j];
+    L.a_voff[j] = (on && a_load_k<F8>(wave, R::APB, j, lane) >= kin) ? kOobOffset : L.a_voff[j];
 }
 
 // Per-lane LDS byte offsets of the fragment reads: A fragment i of step ks at
 // a_rd[ks] + i*2048 within its slot; the two halves of B fragment j at
 // b_rd[j] and b_rd[j] + 8*BN in B slot 0 (LDS byte addresses; slot s adds
 // s times the slot size, an immediate offset of the read).
-template <int BM, int BN, int NW>
+// fp8: A fragment i of step ks is two 16-byte reads, at a_rd[ks] + i*4096 and
+// a_d further (the next chunk, +-16 bytes under the swizzle); B fragment j is
+// four transposing reads of 8 rows, at b_rd[j] + q*8*BN.
+template <int BM, int BN, int NW, bool F8>
 struct ReadOffsets {
   uint32_t a_rd[2];
-  uint32_t b_rd[Tile<BM, BN, NW>::FN];
+  uint32_t a_d;
+  uint32_t b_rd[Tile<BM, BN, NW, F8>::FN];
 };
 
-template <int BM, int BN, int NW>
-__device__ __forceinline__ void read_offsets(int wm, int wn, int lane, uint32_t b_ring, ReadOffsets<BM, BN, NW>& o) {
-  using T = Tile<BM, BN, NW>;
+template <int BM, int BN, int NW, bool F8>
+__device__ __forceinline__ void read_offsets(int wm, int wn, int lane, uint32_t b_ring, ReadOffsets<BM, BN, NW, F8>& o) {
+  using T = Tile<BM, BN, NW, F8>;
+  if constexpr (F8) {
+    // A: lane l holds row l%32 of the fragment and K bytes 32*(l/32) .. +31 of
+    // the 64-deep step, i.e. chunks 4ks + 2h and 4ks + 2h + 1 (h = l/32)
+    const int row = wm * T::WTM + (lane & 31), h = lane >> 5;
+    const int swz = (row >> 1) & 7;
 #pragma unroll
-  for (int ks = 0; ks < 2; ++ks) o.a_rd[ks] = (uint32_t)(a_frag_off(wm * T::WTM, lane, ks) * 2);
+    for (int ks = 0; ks < 2; ++ks) o.a_rd[ks] = (uint32_t)(row * 128 + 16 * ((4 * ks + 2 * h) ^ swz));
+    o.a_d = (uint32_t)(16 * ((2 * h + 1) ^ swz) - 16 * ((2 * h) ^ swz));
+    // B: in each group of 16 lanes (g = l/16, m = l%16), lanes 2r and 2r+1 point
+    // at the two 8-byte halves of row r of an 8-row x 16-column block; the
+    // transposing read gives lane m column m of the 8 rows.  Group g covers
+    // columns 16*(g&1) of the fragment and rows 32*(g>>1) of the step, so lane
+    // j + 32h ends with column j, K bytes 32h .. 32h+31 over the four reads.
+    const int g = lane >> 4, m = lane & 15;
+    const int k = 32 * (g >> 1) + (m >> 1);
 #pragma unroll
-  for (int j = 0; j < T::FN; ++j) o.b_rd[j] = b_ring + (uint32_t)(b_frag_off<BN>(wn * T::WTN, lane, 0, j) * 2);
+    for (int j = 0; j < T::FN; ++j) {
+      const int n = wn * T::WTN + 32 * j + 16 * (g & 1) + 8 * (m & 1);
+      o.b_rd[j] = b_ring + (uint32_t)(k * BN + 16 * ((n >> 4) ^ b_swz8(k)) + (n & 15));
+    }
+  } else {
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) o.a_rd[ks] = (uint32_t)(a_frag_off(wm * T::WTM, lane, ks) * 2);
+    o.a_d = 0;
+#pragma unroll
+    for (int j = 0; j < T::FN; ++j) o.b_rd[j] = b_ring + (uint32_t)(b_frag_off<BN>(wn * T::WTN, lane, 0, j) * 2);
+  }
+}
+
+typedef __attribute__((address_space(3))) i32x4 lds_i32x4;
+typedef __attribute__((address_space(3))) i32x2 lds_i32x2;
+
+// fp8 operand pieces: half p of A fragment i, quarter q of B fragment j.
+__device__ __forceinline__ void read_a8(uint32_t a_base, uint32_t a_d, int i, int p, i32x8& f) {
+  const i32x4 v = *(const lds_i32x4*)(uintptr_t)(a_base + (uint32_t)(i * 32 * 128) + (p ? a_d : 0u));
+  f[4 * p + 0] = v[0];
+  f[4 * p + 1] = v[1];
+  f[4 * p + 2] = v[2];
+  f[4 * p + 3] = v[3];
+}
+template <int BN>
+__device__ __forceinline__ void read_b8(uint32_t addr, int q, i32x8& f) {
+  const i32x2 v = __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_i32x2*)(uintptr_t)(addr + (uint32_t)(q * 8 * BN)));
+  f[2 * q] = v[0];
+  f[2 * q + 1] = v[1];
 }
 
 // Read item t of a step, in the order the next step's MFMAs consume them:
 // A0, B0, B1, .., B(FN-1), A1, .., A(FM-1).
-template <int BM, int BN, int NW>
-__device__ __forceinline__ void read_item(int t, uint32_t a_base, uint32_t b_slot, const uint32_t* b_rd,
-                                          Frags<BM, BN, NW>& f) {
-  using T = Tile<BM, BN, NW>;
+template <int BM, int BN, int NW, bool F8>
+__device__ __forceinline__ void read_item(int t, uint32_t a_base, uint32_t a_d, uint32_t b_slot, const uint32_t* b_rd,
+                                          Frags<BM, BN, NW, F8>& f) {
+  using T = Tile<BM, BN, NW, F8>;
+  if constexpr (F8) {
+    if (t == 0 || t > T::FN) {
+      const int i = t == 0 ? 0 : t - T::FN;
+      read_a8(a_base, a_d, i, 0, f.a[i]);
+      read_a8(a_base, a_d, i, 1, f.a[i]);
+    } else {
+      const int j = t - 1;
+      const uint32_t b_addr = b_slot + b_rd[j];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) read_b8<BN>(b_addr, q, f.b[j]);
+    }
+  } else {
   if (t == 0 || t > T::FN) {
     const int i = t == 0 ? 0 : t - T::FN;
     f.a[i] = *(lds_bf16x8*)(uintptr_t)(a_base + (uint32_t)(i * 16 * kBK * 2));
@@ -376,6 +469,7 @@ __device__ __forceinline__ void read_item(int t, uint32_t a_base, uint32_t b_slo
     const i16x8 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
     f.b[j] = __builtin_bit_cast(bf16x8, v);
   }
+  }
 }
 
 // Loads of one A block or one B stage: descriptor and M0 of this wave's first segment.
@@ -385,8 +479,8 @@ struct SlotDma {
 };
 
 // Load pair q (loads 2q, 2q+1) of an A block (OP 1) or a B stage (OP 2).
-template <int BM, int BN, int NW, int OP, int Q>
-__device__ __forceinline__ void dma_pair(const SlotDma& d, const RingLanes<BM, BN, NW>& L) {
+template <int BM, int BN, int NW, bool F8, int OP, int Q>
+__device__ __forceinline__ void dma_pair(const SlotDma& d, const RingLanes<BM, BN, NW, F8>& L) {
   constexpr int j = 2 * Q;
   if constexpr (OP == 1)
     dma16_pair<(j & 3) * 1024>(d.rsrc, d.m0 + (uint32_t)((j >> 2) * 4096), L.a_voff[j], L.a_voff[j + 1]);
@@ -395,11 +489,11 @@ __device__ __forceinline__ void dma_pair(const SlotDma& d, const RingLanes<BM, B
 }
 
 // All loads of an A block (OP 1) or a B stage (OP 2).
-template <int BM, int BN, int NW, int OP>
-__device__ __forceinline__ void dma_all(const SlotDma& d, const RingLanes<BM, BN, NW>& L) {
-  using R = Ring<BM, BN, NW>;
+template <int BM, int BN, int NW, bool F8, int OP>
+__device__ __forceinline__ void dma_all(const SlotDma& d, const RingLanes<BM, BN, NW, F8>& L) {
+  using R = Ring<BM, BN, NW, F8>;
   [&]<int... q>(std::integer_sequence<int, q...>) {
-    (dma_pair<BM, BN, NW, OP, q>(d, L), ...);
+    (dma_pair<BM, BN, NW, F8, OP, q>(d, L), ...);
   }(std::make_integer_sequence<int, (OP == 1 ? R::APB : R::BPW) / 2>{});
 }
 
@@ -413,13 +507,15 @@ __device__ __forceinline__ void dma_all(const SlotDma& d, const RingLanes<BM, BN
 //   loads:  each load pair becomes three operations (set M0, load, load) in
 //           consecutive groups from evenly spaced starting groups, so that the
 //           MFMA between M0 and the first load covers the wait M0 needs.
-template <int BM, int BN, int NW, int OP>
+template <int BM, int BN, int NW, bool F8, int OP>
 struct StepPlan {
-  using T = Tile<BM, BN, NW>;
+  using T = Tile<BM, BN, NW, F8>;
   static constexpr int G = T::FM * T::FN;
-  static constexpr int NR = T::FM + 2 * T::FN;
-  static constexpr int NP0 = OP == 1 ? Ring<BM, BN, NW>::APB / 2 : Ring<BM, BN, NW>::BPW / 2;   // pairs from d0
-  static constexpr int NP1 = OP == 1 ? 0 : Ring<BM, BN, NW>::BPW / 2;                      // pairs from d1
+  // fragment reads of the next step: bf16 one A read and two B reads per
+  // fragment; fp8 two A reads and four B reads per fragment
+  static constexpr int NR = F8 ? 2 * T::FM + 4 * T::FN : T::FM + 2 * T::FN;
+  static constexpr int NP0 = OP == 1 ? Ring<BM, BN, NW, F8>::APB / 2 : Ring<BM, BN, NW, F8>::BPW / 2;   // pairs from d0
+  static constexpr int NP1 = OP == 1 ? 0 : Ring<BM, BN, NW, F8>::BPW / 2;                      // pairs from d1
   static constexpr int NP = NP0 + NP1;
   static constexpr int ND = 3 * NP;
   // the B step opens with G0 groups of MFMAs alone and then waits at the
@@ -440,7 +536,7 @@ struct StepPlan {
   // groups that issue neither a read nor a load operation (nor, in the A
   // step, one of the K-mask selects of the first APB groups)
   static constexpr bool busy(int g) {
-    if (OP == 1 && g < Ring<BM, BN, NW>::APB) return true;
+    if (OP == 1 && g < Ring<BM, BN, NW, F8>::APB) return true;
     for (int r = 0; r < NR; ++r)
       if (read_group(r) == g) return true;
     for (int o = 0; o < ND; ++o)
@@ -462,22 +558,37 @@ struct StepPlan {
     }
     return (s * G) / ns;
   }
-  static_assert(NR <= G - G0, "one read per group");
+  // bf16: at most one read beside each 16-cycle MFMA; fp8: two beside each
+  // 64-cycle MFMA
+  static_assert(NR <= (F8 ? 2 : 1) * (G - G0), "reads per group");
   static_assert(ND == 0 || dma_group(ND - 1) < G, "loads fit in the step");
 };
 
 // Per-step state of the split B reads: address and low half of each fragment.
-template <int BM, int BN, int NW>
+template <int BM, int BN, int NW, bool F8>
 struct BReads {
-  uint32_t addr[Tile<BM, BN, NW>::FN];
-  i16x4 lo[Tile<BM, BN, NW>::FN];
+  uint32_t addr[Tile<BM, BN, NW, F8>::FN];
+  i16x4 lo[Tile<BM, BN, NW, F8>::FN];
+  uint32_t a_d;   // fp8: offset of the second half of an A fragment
 };
 
-template <int BM, int BN, int NW, int OP, int r>
-__device__ __forceinline__ void step_read(uint32_t a_base, uint32_t b_slot, const uint32_t* b_rd, BReads<BM, BN, NW>& br,
-                                          Frags<BM, BN, NW>& nxt) {
-  using T = Tile<BM, BN, NW>;
-  if constexpr (r == 0 || r > 2 * T::FN) {
+template <int BM, int BN, int NW, bool F8, int OP, int r>
+__device__ __forceinline__ void step_read(uint32_t a_base, uint32_t b_slot, const uint32_t* b_rd, BReads<BM, BN, NW, F8>& br,
+                                          Frags<BM, BN, NW, F8>& nxt) {
+  using T = Tile<BM, BN, NW, F8>;
+  if constexpr (F8) {
+    // A0 (halves 0, 1), B0 .. B(FN-1) (quarters 0..3 each), A1 .. A(FM-1)
+    if constexpr (r < 2) {
+      read_a8(a_base, br.a_d, 0, r, nxt.a[0]);
+    } else if constexpr (r < 2 + 4 * T::FN) {
+      constexpr int j = (r - 2) / 4, q = (r - 2) % 4;
+      if constexpr (q == 0) br.addr[j] = b_slot + b_rd[j];
+      read_b8<BN>(br.addr[j], q, nxt.b[j]);
+    } else {
+      constexpr int i = 1 + (r - 2 - 4 * T::FN) / 2, h = (r - 2 - 4 * T::FN) % 2;
+      read_a8(a_base, br.a_d, i, h, nxt.a[i]);
+    }
+  } else if constexpr (r == 0 || r > 2 * T::FN) {
     constexpr int i = r == 0 ? 0 : r - 2 * T::FN;
     nxt.a[i] = *(lds_bf16x8*)(uintptr_t)(a_base + (uint32_t)(i * 16 * kBK * 2));
   } else if constexpr ((r - 1) % 2 == 0) {
@@ -493,18 +604,18 @@ __device__ __forceinline__ void step_read(uint32_t a_base, uint32_t b_slot, cons
   }
 }
 
-template <int BM, int BN, int NW, int OP, int g, int... r>
+template <int BM, int BN, int NW, bool F8, int OP, int g, int... r>
 __device__ __forceinline__ void group_reads(uint32_t a_base, uint32_t b_slot, const uint32_t* b_rd,
-                                            BReads<BM, BN, NW>& br, Frags<BM, BN, NW>& nxt, std::integer_sequence<int, r...>) {
-  using P = StepPlan<BM, BN, NW, OP>;
-  ((void)(P::read_group(r) == g ? (step_read<BM, BN, NW, OP, r>(a_base, b_slot, b_rd, br, nxt), 0) : 0), ...);
+                                            BReads<BM, BN, NW, F8>& br, Frags<BM, BN, NW, F8>& nxt, std::integer_sequence<int, r...>) {
+  using P = StepPlan<BM, BN, NW, F8, OP>;
+  ((void)(P::read_group(r) == g ? (step_read<BM, BN, NW, F8, OP, r>(a_base, b_slot, b_rd, br, nxt), 0) : 0), ...);
 }
 
 // Load operation o of a step: o = 3q + k for load pair q (k 0: set M0, k 1
 // and 2: the pair's loads).
-template <int BM, int BN, int NW, int OP, int o>
-__device__ __forceinline__ void step_dma(const SlotDma& d0, const SlotDma& d1, const RingLanes<BM, BN, NW>& L) {
-  using P = StepPlan<BM, BN, NW, OP>;
+template <int BM, int BN, int NW, bool F8, int OP, int o>
+__device__ __forceinline__ void step_dma(const SlotDma& d0, const SlotDma& d1, const RingLanes<BM, BN, NW, F8>& L) {
+  using P = StepPlan<BM, BN, NW, F8, OP>;
   constexpr int q = o / 3, k = o % 3;
   constexpr bool first = q < P::NP0;
   constexpr int qq = first ? q : q - P::NP0;
@@ -521,44 +632,47 @@ __device__ __forceinline__ void step_dma(const SlotDma& d0, const SlotDma& d1, c
   }
 }
 
-template <int BM, int BN, int NW, int OP, int g, int... o>
-__device__ __forceinline__ void group_dma(const SlotDma& d0, const SlotDma& d1, const RingLanes<BM, BN, NW>& L,
+template <int BM, int BN, int NW, bool F8, int OP, int g, int... o>
+__device__ __forceinline__ void group_dma(const SlotDma& d0, const SlotDma& d1, const RingLanes<BM, BN, NW, F8>& L,
                                           std::integer_sequence<int, o...>) {
-  using P = StepPlan<BM, BN, NW, OP>;
-  ((void)(P::dma_group(o) == g ? (step_dma<BM, BN, NW, OP, o>(d0, d1, L), 0) : 0), ...);
+  using P = StepPlan<BM, BN, NW, F8, OP>;
+  ((void)(P::dma_group(o) == g ? (step_dma<BM, BN, NW, F8, OP, o>(d0, d1, L), 0) : 0), ...);
 }
 
-template <int BM, int BN, int NW, int OP, int g, typename X>
-__device__ __forceinline__ void ring_group(Acc<BM, BN, NW>& acc, const Frags<BM, BN, NW>& cur, Frags<BM, BN, NW>& nxt,
+template <int BM, int BN, int NW, bool F8, int OP, int g, typename X>
+__device__ __forceinline__ void ring_group(Acc<BM, BN, NW, F8>& acc, const Frags<BM, BN, NW, F8>& cur, Frags<BM, BN, NW, F8>& nxt,
                                            uint32_t a_base, uint32_t b_slot, const uint32_t* b_rd,
-                                           BReads<BM, BN, NW>& br, const SlotDma& d0, const SlotDma& d1,
-                                           const RingLanes<BM, BN, NW>& L, X& ex) {
-  using T = Tile<BM, BN, NW>;
-  using P = StepPlan<BM, BN, NW, OP>;
+                                           BReads<BM, BN, NW, F8>& br, const SlotDma& d0, const SlotDma& d1,
+                                           const RingLanes<BM, BN, NW, F8>& L, X& ex) {
+  using T = Tile<BM, BN, NW, F8>;
+  using P = StepPlan<BM, BN, NW, F8, OP>;
   constexpr int i = g / T::FN, j = g % T::FN;
-  acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(cur.b[j], cur.a[i], acc[i][j], 0, 0, 0);
+  if constexpr (F8)   // fp8 E4M3 x E4M3 (formats 0, 0), unit scales (E8M0 127)
+    acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(cur.b[j], cur.a[i], acc[i][j], 0, 0, 0, 127, 0, 127);
+  else
+    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(cur.b[j], cur.a[i], acc[i][j], 0, 0, 0);
   if constexpr (OP == 2 && g == P::G0) {
     // the block's barrier: A block b+1 and B stages x0+2, x0+3 have landed for
     // every wave (only the A block loaded in the A step may be in flight), and
     // every wave's reads issued in the A step are done (among them the last
     // reads of the B slot this step loads into, and of the A slot the next A
     // step loads into)
-    wait_vmem_at_most<Ring<BM, BN, NW>::IN_FLIGHT>();
+    wait_vmem_at_most<Ring<BM, BN, NW, F8>::IN_FLIGHT>();
     wait_lds_all();
     __syncthreads();
   }
-  group_reads<BM, BN, NW, OP, g>(a_base, b_slot, b_rd, br, nxt, std::make_integer_sequence<int, P::NR>{});
-  group_dma<BM, BN, NW, OP, g>(d0, d1, L, std::make_integer_sequence<int, P::ND>{});
+  group_reads<BM, BN, NW, F8, OP, g>(a_base, b_slot, b_rd, br, nxt, std::make_integer_sequence<int, P::NR>{});
+  group_dma<BM, BN, NW, F8, OP, g>(d0, d1, L, std::make_integer_sequence<int, P::ND>{});
   ex.template operator()<g>();
   __builtin_amdgcn_sched_barrier(0);
 }
 
-template <int BM, int BN, int NW, int OP, typename X, int... g>
-__device__ __forceinline__ void ring_groups(Acc<BM, BN, NW>& acc, const Frags<BM, BN, NW>& cur, Frags<BM, BN, NW>& nxt,
+template <int BM, int BN, int NW, bool F8, int OP, typename X, int... g>
+__device__ __forceinline__ void ring_groups(Acc<BM, BN, NW, F8>& acc, const Frags<BM, BN, NW, F8>& cur, Frags<BM, BN, NW, F8>& nxt,
                                             uint32_t a_base, uint32_t b_slot, const uint32_t* b_rd,
-                                            BReads<BM, BN, NW>& br, const SlotDma& d0, const SlotDma& d1,
-                                            const RingLanes<BM, BN, NW>& L, X& ex, std::integer_sequence<int, g...>) {
-  (ring_group<BM, BN, NW, OP, g>(acc, cur, nxt, a_base, b_slot, b_rd, br, d0, d1, L, ex), ...);
+                                            BReads<BM, BN, NW, F8>& br, const SlotDma& d0, const SlotDma& d1,
+                                            const RingLanes<BM, BN, NW, F8>& L, X& ex, std::integer_sequence<int, g...>) {
+  (ring_group<BM, BN, NW, F8, OP, g>(acc, cur, nxt, a_base, b_slot, b_rd, br, d0, d1, L, ex), ...);
 }
 
 // One 32-deep step with a fixed instruction order (the plan above): MFMAs of
@@ -567,14 +681,15 @@ __device__ __forceinline__ void ring_groups(Acc<BM, BN, NW>& acc, const Frags<BM
 // (ex.operator()<g>() runs in group g).  The groups are generated as
 // straight-line code (a loop this long is not always unrolled, and the
 // accumulators must stay in registers).
-template <int BM, int BN, int NW, int OP, typename X>
-__device__ __forceinline__ void ring_step(Acc<BM, BN, NW>& acc, const Frags<BM, BN, NW>& cur, Frags<BM, BN, NW>& nxt,
-                                          uint32_t a_base, uint32_t b_slot, const ReadOffsets<BM, BN, NW>& o,
-                                          const SlotDma& d0, const SlotDma& d1, const RingLanes<BM, BN, NW>& L,
+template <int BM, int BN, int NW, bool F8, int OP, typename X>
+__device__ __forceinline__ void ring_step(Acc<BM, BN, NW, F8>& acc, const Frags<BM, BN, NW, F8>& cur, Frags<BM, BN, NW, F8>& nxt,
+                                          uint32_t a_base, uint32_t b_slot, const ReadOffsets<BM, BN, NW, F8>& o,
+                                          const SlotDma& d0, const SlotDma& d1, const RingLanes<BM, BN, NW, F8>& L,
                                           X&& ex) {
-  using T = Tile<BM, BN, NW>;
-  BReads<BM, BN, NW> br;
-  ring_groups<BM, BN, NW, OP>(acc, cur, nxt, a_base, b_slot, o.b_rd, br, d0, d1, L, ex,
+  using T = Tile<BM, BN, NW, F8>;
+  BReads<BM, BN, NW, F8> br;
+  br.a_d = o.a_d;
+  ring_groups<BM, BN, NW, F8, OP>(acc, cur, nxt, a_base, b_slot, o.b_rd, br, d0, d1, L, ex,
                           std::make_integer_sequence<int, T::FM * T::FN>{});
 }
 
@@ -620,18 +735,18 @@ __device__ __forceinline__ uint32_t b_stage_limit(const RingAddr& ra, int x) {
 // outside the B descriptors' ranges and read zeros; A block nb-1 is loaded with
 // its lanes past K masked (selects on the first groups of the step that issues
 // those loads, or in the prologue when nb <= D).
-template <int BM, int BN, int NW>
+template <int BM, int BN, int NW, bool F8>
 __device__ __forceinline__ void main_loop_ring(const RingAddr& ra, int nb, int64_t kin_last,
-                                               const ReadOffsets<BM, BN, NW>& o, RingLanes<BM, BN, NW>& L, int lane,
-                                               Acc<BM, BN, NW>& acc) {
-  using R = Ring<BM, BN, NW>;
-  using T = Tile<BM, BN, NW>;
-  using P1 = StepPlan<BM, BN, NW, 1>;
-  using P2 = StepPlan<BM, BN, NW, 2>;
+                                               const ReadOffsets<BM, BN, NW, F8>& o, RingLanes<BM, BN, NW, F8>& L, int lane,
+                                               Acc<BM, BN, NW, F8>& acc) {
+  using R = Ring<BM, BN, NW, F8>;
+  using T = Tile<BM, BN, NW, F8>;
+  using P1 = StepPlan<BM, BN, NW, F8, 1>;
+  using P2 = StepPlan<BM, BN, NW, F8, 2>;
   constexpr int D = R::D;
   constexpr uint32_t BB = (uint32_t)R::B_BYTES;
   const int wave = ra.wave;
-  const bool masked = kin_last < kBK;
+  const bool masked = kin_last < block_k<F8>();
   const uint32_t a_m0w = ra.lds0 + (uint32_t)(wave * R::APB * 1024);            // this wave's segment, A slot 0
   const uint32_t b_m0w = ra.lds0 + (uint32_t)(R::B_OFF + wave * R::BPW * 1024);  // this wave's segment, B slot 0
   auto a_dma = [&](uint64_t addr, int slot, uint32_t lim) {
@@ -651,15 +766,15 @@ __device__ __forceinline__ void main_loop_ring(const RingAddr& ra, int nb, int64
   // B slots 2k, 2k+1), then wait for block 0.  Depth 2 loads block 1 only when
   // there is one; deeper rings load blocks past K with empty ranges.
   if constexpr (D == 2) {
-    if (masked && nb == 1) mask_a_lanes<BM, BN, NW>(L, wave, lane, kin_last);
-    dma_all<BM, BN, NW, 1>(a_dma(ra.a0, 0, kOobOffset), L);
-    dma_all<BM, BN, NW, 2>(b_dma(ra.b0, 0, 0), L);
-    dma_all<BM, BN, NW, 2>(b_dma(ra.b0 + ra.b_step, 1, 1), L);
+    if (masked && nb == 1) mask_a_lanes<BM, BN, NW, F8>(L, wave, lane, kin_last);
+    dma_all<BM, BN, NW, F8, 1>(a_dma(ra.a0, 0, kOobOffset), L);
+    dma_all<BM, BN, NW, F8, 2>(b_dma(ra.b0, 0, 0), L);
+    dma_all<BM, BN, NW, F8, 2>(b_dma(ra.b0 + ra.b_step, 1, 1), L);
     if (nb > 1) {
-      if (masked && nb == 2) mask_a_lanes<BM, BN, NW>(L, wave, lane, kin_last);
-      dma_all<BM, BN, NW, 1>(a_dma(ra.a0 + kBK * 2, 1, kOobOffset), L);
-      dma_all<BM, BN, NW, 2>(b_dma(ra.b0 + 2 * ra.b_step, 2, 2), L);
-      dma_all<BM, BN, NW, 2>(b_dma(ra.b0 + 3 * ra.b_step, 3, 3), L);
+      if (masked && nb == 2) mask_a_lanes<BM, BN, NW, F8>(L, wave, lane, kin_last);
+      dma_all<BM, BN, NW, F8, 1>(a_dma(ra.a0 + kBK * 2, 1, kOobOffset), L);
+      dma_all<BM, BN, NW, F8, 2>(b_dma(ra.b0 + 2 * ra.b_step, 2, 2), L);
+      dma_all<BM, BN, NW, F8, 2>(b_dma(ra.b0 + 3 * ra.b_step, 3, 3), L);
       wait_vmem_at_most<R::APB + 2 * R::BPW>();
     } else {
       wait_vmem_at_most<0>();
@@ -667,16 +782,16 @@ __device__ __forceinline__ void main_loop_ring(const RingAddr& ra, int nb, int64
   } else {
 #pragma unroll
     for (int k = 0; k < D; ++k) {
-      if (masked) mask_a_lanes_if<BM, BN, NW>(L, wave, lane, kin_last, k == nb - 1);
-      dma_all<BM, BN, NW, 1>(a_dma(ra.a0 + (uint64_t)k * (kBK * 2), k, k < nb ? (uint32_t)kOobOffset : 0u), L);
-      dma_all<BM, BN, NW, 2>(b_dma(ra.b0 + (uint64_t)(2 * k) * ra.b_step, 2 * k, 2 * k), L);
-      dma_all<BM, BN, NW, 2>(b_dma(ra.b0 + (uint64_t)(2 * k + 1) * ra.b_step, 2 * k + 1, 2 * k + 1), L);
+      if (masked) mask_a_lanes_if<BM, BN, NW, F8>(L, wave, lane, kin_last, k == nb - 1);
+      dma_all<BM, BN, NW, F8, 1>(a_dma(ra.a0 + (uint64_t)k * (kBK * 2), k, k < nb ? (uint32_t)kOobOffset : 0u), L);
+      dma_all<BM, BN, NW, F8, 2>(b_dma(ra.b0 + (uint64_t)(2 * k) * ra.b_step, 2 * k, 2 * k), L);
+      dma_all<BM, BN, NW, F8, 2>(b_dma(ra.b0 + (uint64_t)(2 * k + 1) * ra.b_step, 2 * k + 1, 2 * k + 1), L);
     }
     wait_vmem_at_most<(D - 1) * (R::APB + 2 * R::BPW)>();
   }
   __syncthreads();
 
-  Frags<BM, BN, NW> f0, f1;
+  Frags<BM, BN, NW, F8> f0, f1;
   {
     const uint32_t as = ra.lds0 + o.a_rd[0];
     // B slot 0, as an opaque register value: with a literal 0 the compiler
@@ -687,7 +802,7 @@ __device__ __forceinline__ void main_loop_ring(const RingAddr& ra, int nb, int64
     // first MFMAs wait only for their own operands on either path into the loop
 #pragma unroll
     for (int t = 0; t < T::FM + T::FN; ++t) {
-      read_item<BM, BN, NW>(t, as, bs0, o.b_rd, f0);
+      read_item<BM, BN, NW, F8>(t, as, o.a_d, bs0, o.b_rd, f0);
       __builtin_amdgcn_sched_barrier(0);
     }
   }
@@ -696,7 +811,7 @@ __device__ __forceinline__ void main_loop_ring(const RingAddr& ra, int nb, int64
   // step loads A block nb-1; for nb <= D the prologue has masked)
   bool mk[R::APB];
 #pragma unroll
-  for (int j = 0; j < R::APB; ++j) mk[j] = a_load_k(wave, R::APB, j, lane) >= kin_last;
+  for (int j = 0; j < R::APB; ++j) mk[j] = a_load_k<F8>(wave, R::APB, j, lane) >= kin_last;
   const int mask_b = masked ? nb - 1 - D : -1;
 
   // scalar state of block b
@@ -712,7 +827,7 @@ __device__ __forceinline__ void main_loop_ring(const RingAddr& ra, int nb, int64
   uint32_t lim0, lim1;
   uint64_t b_nx1;
   for (int b = 0; b < nb; ++b) {
-    ring_step<BM, BN, NW, 1>(acc, f0, f1, ra.lds0 + la0 + o.a_rd[1], lb1, o, da, da, L, [&]<int g>() {
+    ring_step<BM, BN, NW, F8, 1>(acc, f0, f1, ra.lds0 + la0 + o.a_rd[1], lb1, o, da, da, L, [&]<int g>() {
       if constexpr (g < R::APB) {
         if (mnow && mk[g]) L.a_voff[g] = kOobOffset;
       }
@@ -726,7 +841,7 @@ __device__ __forceinline__ void main_loop_ring(const RingAddr& ra, int nb, int64
       if constexpr (g == P1::stage_group(4, 6)) b_nx1 = b_nx + ra.b_step;
       if constexpr (g == P1::stage_group(5, 6)) db1.rsrc = make_rsrc_addr(b_nx1, lim1);
     });
-    ring_step<BM, BN, NW, 2>(acc, f1, f0, ra.lds0 + la1 + o.a_rd[0], lb2, o, db0, db1, L, [&]<int g>() {
+    ring_step<BM, BN, NW, F8, 2>(acc, f1, f0, ra.lds0 + la1 + o.a_rd[0], lb2, o, db0, db1, L, [&]<int g>() {
       if constexpr (g == P2::stage_group(0, 5)) {
         const uint32_t t = la0;
         la0 = la1;
@@ -774,10 +889,10 @@ __device__ __forceinline__ void main_loop_ring(const RingAddr& ra, int nb, int64
 }
 
 // ---- main loop, general path: element loads staged in registers ---------------------------
-template <int BM, int BN, int NW>
+template <int BM, int BN, int NW, bool F8>
 __device__ __forceinline__ void main_loop_staged(const GemmParams& p, uint16_t* smem, int64_t m0,
-                                                 int64_t n0, int kt0, int kt1, int tid, Acc<BM, BN, NW>& acc) {
-  using T = Tile<BM, BN, NW>;
+                                                 int64_t n0, int kt0, int kt1, int tid, Acc<BM, BN, NW, F8>& acc) {
+  using T = Tile<BM, BN, NW, F8>;
   const int lane = tid & 63, wave = tid >> 6;
   const int wm = wave / T::WGN, wn = wave % T::WGN;
   u32x4 ra[T::A_CH], rb[T::B_CH];
@@ -818,9 +933,9 @@ __device__ __forceinline__ void main_loop_staged(const GemmParams& p, uint16_t* 
     const uint16_t* As = smem + buf * (T::A_ELEMS + T::B_ELEMS);
 #pragma unroll
     for (int ks = 0; ks < kBK / 32; ++ks) {
-      Frags<BM, BN, NW> f;
-      load_frags<BM, BN, NW>(As, As + T::A_ELEMS, wm, wn, lane, ks, 32 * ks, f);
-      mma_step<BM, BN, NW>(f, acc);
+      Frags<BM, BN, NW, F8> f;
+      load_frags<BM, BN, NW, F8>(As, As + T::A_ELEMS, wm, wn, lane, ks, 32 * ks, f);
+      mma_step<BM, BN, NW, F8>(f, acc);
     }
     if (more) store_blocks(buf ^ 1);
     __syncthreads();
@@ -845,10 +960,91 @@ __device__ __forceinline__ u32x4 pair_to_row8(const f32x4& x, const f32x4& y) {
   return u32x4{s0[0], s1[0], s0[1], s1[1]};
 }
 
+// Epilogue of the fp8 kernels (MFMA 32x32x64, B fragment first): fragment
+// (i, j) of the wave, lane l, accumulator v holds row 32i + l%32 and column
+// 32j + 8*(v/4) + 4*(l/32) + v%4 -- four runs of 4 consecutive columns.  For
+// bf16 output, runs (g, g+1) are exchanged between the lane halves with
+// v_permlane32_swap so that each lane stores 8 consecutive columns (16 bytes).
 template <int BM, int BN, int NW, bool OUT_BF16>
-__device__ __forceinline__ void store_tile(const GemmParams& p, const Acc<BM, BN, NW>& acc, int64_t m0, int64_t n0,
+__device__ __forceinline__ void store_tile32(const GemmParams& p, const Acc<BM, BN, NW, true>& acc, int64_t m0,
+                                             int64_t n0, int64_t lstride, int wm, int wn, int lane, bool fast,
+                                             bool fast16) {
+  using T = Tile<BM, BN, NW, true>;
+  typedef typename std::conditional<OUT_BF16, __bf16, float>::type OutT;
+  OutT* out = reinterpret_cast<OutT*>(p.out) + lstride;
+  const int h = lane >> 5;
+  const int64_t r0 = m0 + wm * T::WTM + (lane & 31);
+  const int64_t cb = n0 + wn * T::WTN;
+  if (OUT_BF16 && fast16) {
+    typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+#pragma unroll
+    for (int i = 0; i < T::FM; ++i) {
+      OutT* row = out + (r0 + i * 32) * p.ldo + cb + 8 * h;
+#pragma unroll
+      for (int j = 0; j < T::FN; ++j) {
+#pragma unroll
+        for (int g = 0; g < 4; g += 2) {
+          const f32x16& a = acc[i][j];
+          const bf16x4 xb = {(__bf16)a[4 * g], (__bf16)a[4 * g + 1], (__bf16)a[4 * g + 2], (__bf16)a[4 * g + 3]};
+          const bf16x4 yb = {(__bf16)a[4 * g + 4], (__bf16)a[4 * g + 5], (__bf16)a[4 * g + 6], (__bf16)a[4 * g + 7]};
+          const u32x2 xw = __builtin_bit_cast(u32x2, xb), yw = __builtin_bit_cast(u32x2, yb);
+          const auto s0 = __builtin_amdgcn_permlane32_swap(xw[0], yw[0], false, false);
+          const auto s1 = __builtin_amdgcn_permlane32_swap(xw[1], yw[1], false, false);
+          *reinterpret_cast<u32x4*>(row + j * 32 + 8 * g) = u32x4{s0[0], s1[0], s0[1], s1[1]};
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    return;
+  }
+  if (fast) {
+#pragma unroll
+    for (int i = 0; i < T::FM; ++i) {
+      OutT* row = out + (r0 + i * 32) * p.ldo + cb + 4 * h;
+#pragma unroll
+      for (int j = 0; j < T::FN; ++j)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const f32x16& a = acc[i][j];
+          if (OUT_BF16) {
+            const bf16x4 v = {(__bf16)a[4 * g], (__bf16)a[4 * g + 1], (__bf16)a[4 * g + 2], (__bf16)a[4 * g + 3]};
+            *reinterpret_cast<bf16x4*>(row + j * 32 + 8 * g) = v;
+          } else {
+            const f32x4 v = {a[4 * g], a[4 * g + 1], a[4 * g + 2], a[4 * g + 3]};
+            *reinterpret_cast<f32x4*>(row + j * 32 + 8 * g) = v;
+          }
+        }
+      if (OUT_BF16) __builtin_amdgcn_sched_barrier(0);
+    }
+    return;
+  }
+#pragma unroll
+  for (int i = 0; i < T::FM; ++i) {
+    const int64_t r = r0 + i * 32;
+    if (r >= p.M) continue;
+    OutT* row = out + r * p.ldo;
+#pragma unroll
+    for (int j = 0; j < T::FN; ++j)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int64_t c = cb + j * 32 + 8 * g + 4 * h;
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (c + e < p.N) row[c + e] = (OutT)acc[i][j][4 * g + e];
+      }
+    if (OUT_BF16) __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
+template <int BM, int BN, int NW, bool F8, bool OUT_BF16>
+__device__ __forceinline__ void store_tile(const GemmParams& p, const Acc<BM, BN, NW, F8>& acc, int64_t m0, int64_t n0,
                                            int64_t lstride, int wm, int wn, int lane, bool fast, bool fast16) {
-  using T = Tile<BM, BN, NW>;
+  if constexpr (F8) {
+    store_tile32<BM, BN, NW, OUT_BF16>(p, acc, m0, n0, lstride, wm, wn, lane, fast, fast16);
+    return;
+  } else {
+
+  using T = Tile<BM, BN, NW, F8>;
   typedef typename std::conditional<OUT_BF16, __bf16, float>::type OutT;
   OutT* out = reinterpret_cast<OutT*>(p.out) + lstride;
   const int64_t r0 = m0 + wm * T::WTM + (lane & 15);
@@ -904,22 +1100,24 @@ __device__ __forceinline__ void store_tile(const GemmParams& p, const Acc<BM, BN
     }
     if (OUT_BF16) __builtin_amdgcn_sched_barrier(0);
   }
+  }
 }
 
-template <int BM, int BN, int NW, bool OUT_BF16, bool VEC>
+template <int BM, int BN, int NW, bool F8, bool OUT_BF16, bool VEC>
 __global__ __launch_bounds__(NW * 64, 1) void sfc_gemm_kernel(GemmParams p) {
-  using T = Tile<BM, BN, NW>;
+  using T = Tile<BM, BN, NW, F8>;
   static_assert(T::A_CH >= 1 && T::B_CH >= 1, "tile too small for the workgroup");
+  static_assert(!F8 || VEC, "fp8 operands take the fast path only");
   // fast path: the rings of A block and B stage slots; general path: two 64-deep blocks
-  constexpr int kSmem = VEC ? Ring<BM, BN, NW>::ELEMS : 2 * (T::A_ELEMS + T::B_ELEMS);
+  constexpr int kSmem = VEC ? Ring<BM, BN, NW, F8>::ELEMS : 2 * (T::A_ELEMS + T::B_ELEMS);
   __shared__ __attribute__((aligned(16))) uint16_t smem[kSmem];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / T::WGN, wn = wave % T::WGN;
-  ReadOffsets<BM, BN, NW> ro;
-  if constexpr (VEC) read_offsets<BM, BN, NW>(wm, wn, lane, lds_addr(smem) + (uint32_t)Ring<BM, BN, NW>::B_OFF, ro);
+  ReadOffsets<BM, BN, NW, F8> ro;
+  if constexpr (VEC) read_offsets<BM, BN, NW, F8>(wm, wn, lane, lds_addr(smem) + (uint32_t)Ring<BM, BN, NW, F8>::B_OFF, ro);
 
   const int P = gridDim.x;
   const int rank = xcd_rank(blockIdx.x, P);
@@ -957,37 +1155,45 @@ __global__ __launch_bounds__(NW * 64, 1) void sfc_gemm_kernel(GemmParams p) {
     const int kt0 = (int)((unsigned)layer * (unsigned)p.nk / (unsigned)p.layers);
     const int kt1 = (int)((unsigned)(layer + 1) * (unsigned)p.nk / (unsigned)p.layers);
 
-    Acc<BM, BN, NW> acc;
+    Acc<BM, BN, NW, F8> acc;
 #pragma unroll
     for (int i = 0; i < T::FM; ++i)
 #pragma unroll
-      for (int j = 0; j < T::FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int j = 0; j < T::FN; ++j) {
+        if constexpr (F8) acc[i][j] = f32x16{};
+        else acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+      }
 
     if (kt0 < kt1) {
       if constexpr (VEC) {
-        const int64_t k0 = (int64_t)kt0 * kBK;
-        RingLanes<BM, BN, NW> L;
-        ring_lanes<BM, BN, NW>(p, m0, n0, wave, lane_t, L);
+        constexpr int ESZ = F8 ? 1 : 2;          // bytes per element
+        constexpr int SK = stage_k<F8>();
+        const int64_t k0 = (int64_t)kt0 * block_k<F8>();
+        RingLanes<BM, BN, NW, F8> L;
+        ring_lanes<BM, BN, NW, F8>(p, m0, n0, wave, lane_t, L);
         RingAddr ra;
-        ra.a0 = reinterpret_cast<uint64_t>(p.A + m0 * p.lda + k0) - kBias;
-        ra.b0 = reinterpret_cast<uint64_t>(p.B + k0 * p.ldb + n0) - kBias;
-        ra.b_step = (uint64_t)kSK * (uint64_t)p.ldb * 2;
+        const uint8_t* Ab = reinterpret_cast<const uint8_t*>(p.A);
+        const uint8_t* Bb = reinterpret_cast<const uint8_t*>(p.B);
+        ra.a0 = reinterpret_cast<uint64_t>(Ab + (m0 * p.lda + k0) * ESZ) - kBias;
+        ra.b0 = reinterpret_cast<uint64_t>(Bb + (k0 * p.ldb + n0) * ESZ) - kBias;
+        ra.b_step = (uint64_t)SK * (uint64_t)p.ldb * ESZ;
         {
           const int b_rows = (int)(p.K - k0);   // rows of B from the task's first stage to row K
-          ra.x_part = b_rows / kSK;
-          ra.lim_part = (uint32_t)((b_rows % kSK) * (int)(p.ldb * 2) + kBias);
+          ra.x_part = b_rows / SK;
+          ra.lim_part = (uint32_t)((b_rows % SK) * (int)(p.ldb * ESZ) + kBias);
         }
         ra.lds0 = lds_addr(smem);
         ra.wave = wave;
-        main_loop_ring<BM, BN, NW>(ra, kt1 - kt0, p.K - (int64_t)(kt1 - 1) * kBK, ro, L, lane_t, acc);
-      } else {
-        main_loop_staged<BM, BN, NW>(p, smem, m0, n0, kt0, kt1, tid, acc);
+        main_loop_ring<BM, BN, NW, F8>(ra, kt1 - kt0, p.K - (int64_t)(kt1 - 1) * block_k<F8>(), ro, L, lane_t,
+                                       acc);
+      } else if constexpr (!F8) {
+        main_loop_staged<BM, BN, NW, F8>(p, smem, m0, n0, kt0, kt1, tid, acc);
       }
     }
 
     const int64_t lstride = p.out_layer_stride * layer;
     const bool interior = m0 + BM <= p.M && n0 + BN <= p.N;
-    store_tile<BM, BN, NW, OUT_BF16>(p, acc, m0, n0, lstride, wm, wn, lane_t, interior && vec_store,
+    store_tile<BM, BN, NW, F8, OUT_BF16>(p, acc, m0, n0, lstride, wm, wn, lane_t, interior && vec_store,
                                       interior && vec16_store);
   }
 }
@@ -1004,15 +1210,21 @@ __global__ __launch_bounds__(NW * 64, 1) void sfc_gemm_kernel(GemmParams p) {
 static_assert(SFC_WAVES_256x256 == 4 || SFC_WAVES_256x256 == 8, "4 or 8 waves");
 static constexpr int fast_waves(int tile) { return tile == kT256x256 ? SFC_WAVES_256x256 : 4; }
 
-template <int BM, int BN, int NW, bool OB, bool VEC>
+template <int BM, int BN, int NW, bool F8, bool OB, bool VEC>
 static const void* kernel_ptr() {
-  return reinterpret_cast<const void*>(&sfc_gemm_kernel<BM, BN, NW, OB, VEC>);
+  return reinterpret_cast<const void*>(&sfc_gemm_kernel<BM, BN, NW, F8, OB, VEC>);
+}
+
+// fp8 (OCP E4M3) operands: 256x256 blocks, fast path only.
+static const void* select_kernel_f8(int tile, bool ob) {
+  if (tile != kT256x256) return nullptr;
+  return ob ? kernel_ptr<256, 256, 4, true, true, true>() : kernel_ptr<256, 256, 4, true, false, true>();
 }
 
 static const void* select_kernel(int tile, bool ob, bool vec) {
 #define SFC_K(BM_, BN_, NW_)                                                                   \
-  return ob ? (vec ? kernel_ptr<BM_, BN_, NW_, true, true>() : kernel_ptr<BM_, BN_, 4, true, false>()) \
-            : (vec ? kernel_ptr<BM_, BN_, NW_, false, true>() : kernel_ptr<BM_, BN_, 4, false, false>())
+  return ob ? (vec ? kernel_ptr<BM_, BN_, NW_, false, true, true>() : kernel_ptr<BM_, BN_, 4, false, true, false>()) \
+            : (vec ? kernel_ptr<BM_, BN_, NW_, false, false, true>() : kernel_ptr<BM_, BN_, 4, false, false, false>())
   switch (tile) {
     case kT128x128: SFC_K(128, 128, 4);
     case kT256x128: SFC_K(256, 128, 4);
@@ -1026,16 +1238,16 @@ static const void* select_kernel(int tile, bool ob, bool vec) {
 static int threads_of(int tile, bool vec) { return (vec ? fast_waves(tile) : 4) * 64; }
 
 hipError_t launch_gemm(int tile, bool out_bf16, bool vec, const GemmParams& p, int grid,
-                       hipStream_t stream) {
-  const void* k = select_kernel(tile, out_bf16, vec);
+                       hipStream_t stream, bool f8) {
+  const void* k = f8 ? select_kernel_f8(tile, out_bf16) : select_kernel(tile, out_bf16, vec);
   if (!k) return hipErrorInvalidValue;
   GemmParams local = p;
   void* args[] = {&local};
   return hipLaunchKernel(k, dim3(grid), dim3(threads_of(tile, vec)), args, 0, stream);
 }
 
-hipError_t gemm_occupancy(int tile, bool out_bf16, bool vec, int* blocks_per_cu) {
-  const void* k = select_kernel(tile, out_bf16, vec);
+hipError_t gemm_occupancy(int tile, bool out_bf16, bool vec, int* blocks_per_cu, bool f8) {
+  const void* k = f8 ? select_kernel_f8(tile, out_bf16) : select_kernel(tile, out_bf16, vec);
   if (!k) return hipErrorInvalidValue;
   return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, k, threads_of(tile, vec), 0);
 }

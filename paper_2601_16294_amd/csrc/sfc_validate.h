@@ -106,4 +106,28 @@ inline bool vector_loads_ok(const void* A, int64_t lda, const void* B, int64_t l
          ldb < ((int64_t)1 << 22);
 }
 
+// fp8 (OCP E4M3) operands take the 16-byte load path only: 16-byte aligned
+// rows, and K and N ending on whole 16-element chunks.
+inline bool f8_loads_ok(const void* A, int64_t lda, const void* B, int64_t ldb, int64_t K, int64_t N) {
+  return ((uintptr_t)A % 16 == 0) && ((uintptr_t)B % 16 == 0) && (lda % 16 == 0) && (ldb % 16 == 0) &&
+         (K % 16 == 0) && (N % 16 == 0) && lda < ((int64_t)1 << 21) && ldb < ((int64_t)1 << 23);
+}
+
+inline Checked check_gemm_f8_args(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda,
+                                  const void* B, int64_t ldb, const void* C, int64_t ldc,
+                                  int out_type, int ca_layers, int tile, int order, int sched,
+                                  const void* ws, size_t ws_bytes) {
+  Checked c = check_gemm_args(M, N, K, A, lda, B, ldb, C, ldc, out_type, ca_layers, tile, order, sched, ws,
+                              ws_bytes);
+  if (c.code != SFC_OK || M == 0 || N == 0) return c;
+  if (ca_layers == 0)
+    return fail(SFC_ERR_UNSUPPORTED, "fp8 operands need an explicit ca_layers (the model is calibrated for bf16)");
+  if (tile != SFC_TILE_AUTO && tile != SFC_TILE_256x256)
+    return fail(SFC_ERR_UNSUPPORTED, "fp8 operands run on 256x256 blocks");
+  if (K > 0 && !f8_loads_ok(A, lda, B, ldb, K, N))
+    return fail(SFC_ERR_UNSUPPORTED,
+                "fp8 operands need 16-byte aligned A and B and lda, ldb, K, N multiples of 16");
+  return ok();
+}
+
 }  // namespace sfc

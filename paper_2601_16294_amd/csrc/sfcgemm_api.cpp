@@ -25,7 +25,7 @@ struct DeviceState {
   void* ws = nullptr;
   size_t ws_bytes = 0;
   int num_cus = 0;
-  int occupancy[sfc::kNumTiles][2][2] = {};                  // [tile][bf16][vec], 0 = unknown
+  int occupancy[sfc::kNumTiles][2][2][2] = {};               // [tile][bf16 out][vec][fp8 in], 0 = unknown
 };
 
 std::mutex g_mu;
@@ -79,11 +79,11 @@ int get_table(DeviceState& st, int gm, int gn, int order, hipStream_t stream, co
   return SFC_OK;
 }
 
-int get_occupancy(DeviceState& st, int tile, bool ob, bool vec, int* occ) {
-  int& o = st.occupancy[tile][ob][vec];
+int get_occupancy(DeviceState& st, int tile, bool ob, bool vec, int* occ, bool f8 = false) {
+  int& o = st.occupancy[tile][ob][vec][f8];
   if (o == 0) {
     int v = 0;
-    hipError_t e = sfc::gemm_occupancy(tile, ob, vec, &v);
+    hipError_t e = sfc::gemm_occupancy(tile, ob, vec, &v, f8);
     if (e != hipSuccess) return hip_fail(e, "occupancy query");
     o = v < 1 ? 1 : v;
   }
@@ -107,10 +107,27 @@ struct Plan {
 };
 
 int make_plan(DeviceState& st, int64_t M, int64_t N, int64_t K, const void* A, int64_t lda,
-              const void* B, int64_t ldb, bool ob, int ca_layers, int tile_api, Plan* pl) {
+              const void* B, int64_t ldb, bool ob, int ca_layers, int tile_api, Plan* pl, bool f8 = false) {
+  int rc = SFC_OK;
+  if (f8) {
+    // fp8 operands (checked by check_gemm_f8_args): 256x256 blocks, 128-deep K
+    // blocks, the given layer count
+    pl->vec = true;
+    pl->tile = sfc::kT256x256;
+    pl->ce = sfc::effective_layers(K, ca_layers, 128);
+    pl->bm = pl->bn = 256;
+    pl->gm = (int)sfc::ceil_div(M, 256);
+    pl->gn = (int)sfc::ceil_div(N, 256);
+    pl->nk = (int)(K > 0 ? sfc::ceil_div(K, 128) : 0);
+    rc = get_occupancy(st, pl->tile, ob && pl->ce == 1, true, &pl->occ, true);
+    if (rc != SFC_OK) return rc;
+    const int64_t tasks = (int64_t)pl->gm * pl->gn * pl->ce;
+    const int64_t slots = (int64_t)st.num_cus * pl->occ;
+    pl->grid = (int)(tasks < slots ? tasks : slots);
+    return SFC_OK;
+  }
   // the fast path needs at least one K block per task
   pl->vec = K > 0 && sfc::vector_loads_ok(A, lda, B, ldb, K, N);
-  int rc = SFC_OK;
   if (tile_api == SFC_TILE_AUTO || ca_layers == SFC_CA_AUTO) {
     // the analytical model evaluates the free knobs (block shape, layers)
     int occ[sfc::kNumTiles];
@@ -144,9 +161,12 @@ int make_plan(DeviceState& st, int64_t M, int64_t N, int64_t K, const void* A, i
 
 int gemm_impl(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* B,
               int64_t ldb, void* C, int64_t ldc, int out_type, int ca_layers, int tile, int order,
-              int sched, void* ws, size_t ws_bytes, void* stream_ptr) {
-  const sfc::Checked chk = sfc::check_gemm_args(M, N, K, A, lda, B, ldb, C, ldc, out_type, ca_layers,
-                                                tile, order, sched, ws, ws_bytes);
+              int sched, void* ws, size_t ws_bytes, void* stream_ptr, bool f8 = false) {
+  const sfc::Checked chk =
+      f8 ? sfc::check_gemm_f8_args(M, N, K, A, lda, B, ldb, C, ldc, out_type, ca_layers, tile, order, sched, ws,
+                                   ws_bytes)
+         : sfc::check_gemm_args(M, N, K, A, lda, B, ldb, C, ldc, out_type, ca_layers, tile, order, sched, ws,
+                                ws_bytes);
   if (chk.code != SFC_OK) return set_error(chk.code, chk.msg);
   if (M == 0 || N == 0) return SFC_OK;
   hipStream_t stream = reinterpret_cast<hipStream_t>(stream_ptr);
@@ -157,7 +177,7 @@ int gemm_impl(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const
   int rc = device_state(&st);
   if (rc != SFC_OK) return rc;
   Plan pl;
-  rc = make_plan(*st, M, N, K, A, lda, B, ldb, ob, ca_layers, tile, &pl);
+  rc = make_plan(*st, M, N, K, A, lda, B, ldb, ob, ca_layers, tile, &pl, f8);
   if (rc != SFC_OK) return rc;
   const int32_t* table = nullptr;
   rc = get_table(*st, pl.gm, pl.gn, order, stream, &table);
@@ -199,7 +219,7 @@ int gemm_impl(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const
   p.tasks = (int64_t)pl.gm * pl.gn * pl.ce;
   p.sched = sched;
   p.pad_ = 0;
-  hipError_t e = sfc::launch_gemm(pl.tile, ob && pl.ce == 1, pl.vec, p, pl.grid, stream);
+  hipError_t e = sfc::launch_gemm(pl.tile, ob && pl.ce == 1, pl.vec, p, pl.grid, stream, f8);
   if (e != hipSuccess) return hip_fail(e, "GEMM launch");
   if (pl.ce > 1) {
     e = sfc::launch_reduce(W, pl.ce, M, N, C, ldc, ob, stream);
@@ -256,6 +276,13 @@ int sfc_gemm_ex(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, con
                 int sched, void* ws, size_t ws_bytes, void* stream) {
   return gemm_impl(M, N, K, A, lda, B, ldb, C, ldc, out_type, ca_layers, tile, order, sched, ws,
                    ws_bytes, stream);
+}
+
+int sfc_gemm_f8_ex(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* B,
+                   int64_t ldb, void* C, int64_t ldc, int out_type, int ca_layers, int tile, int order,
+                   int sched, void* ws, size_t ws_bytes, void* stream) {
+  return gemm_impl(M, N, K, A, lda, B, ldb, C, ldc, out_type, ca_layers, tile, order, sched, ws,
+                   ws_bytes, stream, true);
 }
 
 int sfc_gemm(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* B, int64_t ldb,

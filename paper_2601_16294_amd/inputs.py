@@ -54,6 +54,33 @@ def draw(rows: int, cols: int, dist: Tuple, seed: int, ld: Optional[int] = None)
     return out
 
 
+NAN_E4M3 = 0x7F
+
+
+def draw_e4m3(rows: int, cols: int, dist: Tuple, seed: int, ld: Optional[int] = None) -> np.ndarray:
+    """A rows x ld uint8 array of OCP FP8 E4M3 codes (drawn in fp32 as in draw()
+    and converted by torch's float8_e4m3fn cast, round to nearest even);
+    columns >= cols hold the NaN code."""
+    ld = cols if ld is None else ld
+    if ld < cols:
+        raise ValueError("ld < cols")
+    rng = np.random.default_rng(seed)
+    kind = dist[0]
+    if kind == "uniform":
+        x = rng.uniform(dist[1], dist[2], size=(rows, cols)).astype(np.float32)
+    elif kind == "normal":
+        x = rng.normal(dist[1], dist[2], size=(rows, cols)).astype(np.float32)
+    elif kind == "int":
+        x = rng.integers(dist[1], dist[2] + 1, size=(rows, cols)).astype(np.float32)
+    else:
+        raise ValueError(kind)
+    out = np.full((rows, ld), NAN_E4M3, dtype=np.uint8)
+    if rows and cols:
+        t = torch.from_numpy(np.ascontiguousarray(x)).to(torch.float8_e4m3fn)
+        out[:, :cols] = t.view(torch.uint8).numpy()
+    return out
+
+
 @dataclass
 class Gemm:
     M: int

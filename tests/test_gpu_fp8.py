@@ -1,0 +1,118 @@
+"""Parity of the fp8 (OCP E4M3) GEMM path (sfc_gemm_f8_ex, through the C ABI)
+with the fp64 oracle over the decoded operands: ragged M, K tails inside a
+128-deep block, several layer counts, both output types, exact integer
+inputs, the bf16 output as RNE of the fp32 output, and the argument checks."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import bf16 as obf16
+from oracle import check as ocheck
+from oracle import fp8 as of8
+from oracle import gemm as ogemm
+from paper_2601_16294_amd.inputs import NAN_E4M3, draw_e4m3
+from gpu_util import raw_bits, sg, to_host
+
+pytestmark = pytest.mark.gpu
+
+
+def up8(bits):
+    return sg().to_device_u8(bits)
+
+
+def ref(A8, B8, M, N, K):
+    A = of8.e4m3_to_bf16_bits(A8[:, :K])
+    B = of8.e4m3_to_bf16_bits(B8[:, :N])
+    return ogemm.gemm_ref_rows(A, B, N, K, K, N, M=M)
+
+
+def run8(A8, B8, M, N, K, out="f32", c=1, ldc=None):
+    ldc = N if ldc is None else ldc
+    dtype = torch.float32 if out == "f32" else torch.bfloat16
+    Cfull = torch.full((M, ldc), float("nan"), dtype=dtype, device="cuda")
+    dA, dB = up8(A8), up8(B8)
+    sg().sfc_gemm_f8_ex(dA[:M, :K], dB[:K, :N], Cfull[:, :N], ca_layers=c)
+    torch.cuda.synchronize()
+    return Cfull
+
+
+SHAPES = [(1, 16, 16), (7, 32, 48), (256, 256, 256), (300, 528, 400), (257, 512, 128), (513, 272, 1040),
+          (130, 1024, 2064)]
+
+
+@pytest.mark.parametrize("M,N,K", SHAPES)
+@pytest.mark.parametrize("out", ["f32", "bf16"])
+def test_ragged_shapes(M, N, K, out):
+    A = draw_e4m3(M, K, ("normal", 0.0, 1.0), M + K)
+    B = draw_e4m3(K, N, ("normal", 0.0, 1.0), N + K + 1)
+    Cr, R = ref(A, B, M, N, K)
+    for c in (1, 3):
+        C = to_host(run8(A, B, M, N, K, out, c))
+        ocheck.assert_gemm_close(C, Cr, R, f"fp8 {M}x{N}x{K} {out} c={c}")
+
+
+@pytest.mark.parametrize("c", [1, 2, 5])
+def test_integer_inputs_exact(c):
+    M, N, K = 300, 272, 1040
+    A = draw_e4m3(M, K, ("int", -4, 4), 31)
+    B = draw_e4m3(K, N, ("int", -4, 4), 32)
+    Ai = of8.e4m3_to_f64(A).astype(np.int64)
+    Bi = of8.e4m3_to_f64(B).astype(np.int64)
+    C = to_host(run8(A, B, M, N, K, "f32", c))
+    assert np.array_equal(C, (Ai @ Bi).astype(np.float64))
+
+
+def test_bf16_output_is_rne_of_f32_output_and_padding_untouched():
+    M, N, K = 333, 528, 656
+    A = draw_e4m3(M, K, ("normal", 0.0, 1.0), 41)
+    B = draw_e4m3(K, N, ("normal", 0.0, 1.0), 42)
+    C32 = run8(A, B, M, N, K, "f32", ldc=544)
+    C16 = run8(A, B, M, N, K, "bf16", ldc=544)
+    want = obf16.f32_to_bf16_rne(C32[:, :N].contiguous().cpu().numpy())
+    assert np.array_equal(raw_bits(C16[:, :N].contiguous()), want)
+    assert np.isnan(to_host(C32)[:, N:]).all() and np.isnan(to_host(C16)[:, N:]).all()
+
+
+def test_lda_ldb_padding_is_never_read():
+    M, N, K = 200, 256, 384
+    A = draw_e4m3(M, K, ("uniform", -1.0, 1.0), 51, ld=400)   # NaN codes beyond K
+    B = draw_e4m3(K, N, ("uniform", -1.0, 1.0), 52, ld=272)   # NaN codes beyond N
+    dA, dB = up8(A), up8(B)
+    C = torch.empty((M, N), dtype=torch.float32, device="cuda")
+    sg().sfc_gemm_f8_ex(dA[:, :K], dB[:, :N], C)
+    torch.cuda.synchronize()
+    Cr, R = ref(A, B, M, N, K)
+    ocheck.assert_gemm_close(to_host(C), Cr, R, "fp8 padded operands")
+
+
+def test_unsupported_arguments_are_rejected():
+    A = up8(np.zeros((64, 48), np.uint8))
+    B = up8(np.zeros((48, 64), np.uint8))
+    C = torch.zeros((64, 64), dtype=torch.float32, device="cuda")
+    with pytest.raises(sg().SfcError) as e:
+        sg().sfc_gemm_f8_ex(A[:, :40], B[:40, :], C)          # K not a multiple of 16
+    assert e.value.code == sg().SFC_ERR_UNSUPPORTED
+    with pytest.raises(sg().SfcError) as e:
+        sg().sfc_gemm_f8_ex(A, B, C, ca_layers=0)            # no model for fp8
+    assert e.value.code == sg().SFC_ERR_UNSUPPORTED
+    with pytest.raises(sg().SfcError) as e:
+        sg().sfc_gemm_f8_ex(A, B, C, tile="128x128")
+    assert e.value.code == sg().SFC_ERR_UNSUPPORTED
+    torch.cuda.synchronize()
+    assert (C == 0).all()
+
+
+@pytest.mark.slow
+def test_full_size_8192_sampled():
+    M = N = K = 8192
+    A = draw_e4m3(M, K, ("normal", 0.0, 1.0), 61)
+    B = draw_e4m3(K, N, ("normal", 0.0, 1.0), 62)
+    C = to_host(run8(A, B, M, N, K, "bf16"))
+    Ab, Bb = of8.e4m3_to_bf16_bits(A), of8.e4m3_to_bf16_bits(B)
+    rng = np.random.default_rng(63)
+    rows, cols = rng.integers(0, M, 2048), rng.integers(0, N, 2048)
+    Cp, Rp = ogemm.gemm_ref_points(Ab, Bb, K, K, N, rows, cols)
+    ocheck.assert_gemm_close(C[rows, cols], Cp, Rp, "fp8 8192^3 points")
+    for r in (0, 4095, 8191):
+        Cr, Rr = ogemm.gemm_ref_rows(Ab, Bb, N, K, K, N, row0=r, nrows=1)
+        ocheck.assert_gemm_close(C[r:r + 1], Cr, Rr, f"fp8 8192^3 row {r}")
