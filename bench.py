@@ -60,7 +60,8 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--order", default="hilbert", choices=["hilbert", "row_major"])
     ap.add_argument("--sched", default="interleaved", choices=["interleaved", "block"])
-    ap.add_argument("--only", default=None, help="run the kernel of one workload K times and exit")
+    ap.add_argument("--only", default=None,
+                    help="run the kernel of one workload (or fp8_square8192) K times and exit")
     ap.add_argument("--sweep", action="store_true", help="also run the 125-shape sweep")
     ap.add_argument("--sweep-reps", type=int, default=3, help="cold repetitions per autotune candidate")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -186,6 +187,16 @@ def main():
         C = torch.empty((g.M, g.N), dtype=dtype, device=dev)
         return A, B, dA, dB, C
 
+    if args.only == "fp8_square8192":
+        from paper_2601_16294_amd.inputs import draw_e4m3
+        a8 = sg.to_device_u8(draw_e4m3(8192, 8192, ("normal", 0.0, 1.0), 2101))
+        b8 = sg.to_device_u8(draw_e4m3(8192, 8192, ("normal", 0.0, 1.0), 2102))
+        c8 = torch.empty((8192, 8192), dtype=torch.bfloat16, device=dev)
+        for _ in range(args.steps):
+            sg.sfc_gemm_f8_ex(a8, b8, c8, stream=stream)
+        torch.cuda.synchronize()
+        log(f"[bench] ran fp8_square8192 {args.steps} times")
+        return
     if args.only:
         ow = W[args.only]
         og = ow.gemms[0]
@@ -267,6 +278,28 @@ def main():
     f8_tf = g.flops / (f8_ms * 1e-3) / 1e12
     fp8 = {"call": "sfc_gemm_f8_ex, E4M3 A and B ~ N(0,1), bf16 out, 256x256 blocks", "ms": round(f8_ms, 4),
            "tflops": round(f8_tf, 1), "peak": PEAK_FP8_TFLOPS, "frac": round(f8_tf / PEAK_FP8_TFLOPS, 4)}
+    # the vendor library on the same E4M3 operands (torch._scaled_mm -> hipBLASLt),
+    # when this torch build offers it: a reference point, not part of the path
+    try:
+        fa = a8.view(torch.float8_e4m3fn)
+        fb = b8.view(torch.float8_e4m3fn).t().contiguous().t()   # column-major B, as the call requires
+        one = torch.ones((), dtype=torch.float32, device=dev)
+        for _ in range(args.warmup):
+            torch._scaled_mm(fa, fb, scale_a=one, scale_b=one, out_dtype=torch.bfloat16)
+        torch.cuda.synchronize()
+        evl = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+        for s0, s1 in evl:
+            s0.record(stream)
+            torch._scaled_mm(fa, fb, scale_a=one, scale_b=one, out_dtype=torch.bfloat16)
+            s1.record(stream)
+        torch.cuda.synchronize()
+        lib8_ms = sum(x.elapsed_time(y) for x, y in evl) / args.steps
+        fp8["library_same_workload"] = {"call": "torch._scaled_mm (hipBLASLt), E4M3 in, bf16 out",
+                                        "ms": round(lib8_ms, 4),
+                                        "tflops": round(g.flops / (lib8_ms * 1e-3) / 1e12, 1)}
+        del fa, fb
+    except (RuntimeError, TypeError) as e:   # not offered by this torch build / device
+        fp8["library_same_workload"] = {"unavailable": str(e)[:120]}
     log(f"[bench] fp8 {fp8}")
     del a8, b8, c8
     torch.cuda.empty_cache()

@@ -1,10 +1,12 @@
-// Persistent bf16 MFMA GEMM for gfx950 whose output blocks are taken in
-// space-filling-curve order, with the communication-avoiding K split.
+// Persistent MFMA GEMM for gfx950 (bf16 operands, or OCP FP8 E4M3 operands)
+// whose output blocks are taken in space-filling-curve order, with the
+// communication-avoiding K split.
 //
 // What it computes (Listing 1, Section II.D): the task space has gm*gn*layers
 // entries; task t is layer l = t / (gm*gn) and curve position s = t % (gm*gn);
 // the curve table maps s to the output block (im, in); layer l contracts the
-// l-th contiguous range of 64-deep K blocks into its own copy of the block.
+// l-th contiguous range of K blocks (64 deep for bf16, 128 for fp8) into its
+// own copy of the block.
 // With one layer the copy is C itself (fp32 or bf16); with several it is an
 // fp32 workspace layer that a separate reduction sums.
 //
@@ -38,6 +40,11 @@
 //   * bf16 output: v_permlane16_swap pairs two fragments so that every lane
 //     stores 8 consecutive columns (16 bytes); a store instruction costs about
 //     the same whatever its width, so this halves the epilogue.
+//   * fp8 operands (F8): the rings hold the same bytes (an A block row is 128
+//     fp8, a B stage 64 rows of BN fp8); each 64-deep step is MFMA 32x32x64
+//     f8f6f4 per 32x32 fragment, fed by two 16-byte A reads and four
+//     ds_read_b64_tr_b8 B reads per fragment, and the 32x32 accumulators are
+//     stored by store_tile32.
 #include <type_traits>
 #include <utility>
 
