@@ -50,7 +50,8 @@ def test_version_and_strings(sg):
     (100, 50, 130, 4, 3 * 100 * 50 * 4),  # three K blocks: three layers
     (100, 50, 0, 4, 0),
     (-1, 5, 5, 2, 0),
-    (5, 5, 500, 0, 8 * 5 * 5 * 4),       # SFC_CA_AUTO: bound for the model's largest count, 8
+    (5, 5, 500, 0, 8 * 5 * 5 * 4),       # SFC_CA_AUTO: the model's largest count (16), capped at the 8 K blocks
+    (5, 5, 1500, 0, 16 * 5 * 5 * 4),     # ... or the largest count itself
     (5, 5, 100, 0, 2 * 5 * 5 * 4),       # ... capped at the K blocks
     (5, 5, 500, -1, 0),
     (5, 5, 500, 65, 0),
@@ -82,7 +83,7 @@ def call_ex(sg, **kw):
     (dict(c=2, K=128, lda=128, ws=1 << 20, wsb=2 * 64 * 64 * 4 - 1), -3),
     (dict(c=2, K=128, lda=128, ws=(1 << 20) + 8, wsb=1 << 20), -2),
     # SFC_CA_AUTO with a caller workspace: it must hold the largest count the
-    # model picks (8 layers, here capped at the 4 K blocks)
+    # model picks (16 layers, here capped at the 4 K blocks)
     (dict(c=0, K=256, lda=256, ws=1 << 20, wsb=4 * 64 * 64 * 4 - 1), -3),
 ])
 def test_invalid_arguments_rejected_before_any_launch(sg, kw, code):
@@ -121,3 +122,35 @@ def test_probe_validation(sg):
     d = ctypes.c_double()
     assert sg.lib.sfc_probe_mfma(1, 0, ctypes.byref(d), ctypes.byref(d)) == -1
     assert sg.lib.sfc_probe_mfma(1, 10, None, ctypes.byref(d)) == -1
+
+
+F8GOOD = dict(M=64, N=64, K=64, A=4096, lda=64, B=8192, ldb=64, C=16384, ldc=64, out=F32, c=1,
+              tile=0, order=0, sched=0, ws=None, wsb=0)
+
+
+def call_f8(sg, **kw):
+    a = dict(F8GOOD)
+    a.update(kw)
+    return sg.lib.sfc_gemm_f8_ex(a["M"], a["N"], a["K"], a["A"], a["lda"], a["B"], a["ldb"], a["C"], a["ldc"],
+                                 a["out"], a["c"], a["tile"], a["order"], a["sched"], a["ws"], a["wsb"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(M=-1), -1), (dict(lda=63), -1), (dict(ldb=63), -1), (dict(A=None), -1), (dict(out=2), -1),
+    (dict(c=65), -1), (dict(tile=5), -1),
+    (dict(K=40, lda=64), -2),                 # K not a multiple of 16
+    (dict(N=40, ldb=64, ldc=64), -2),         # N not a multiple of 16
+    (dict(lda=72), -2), (dict(ldb=72), -2),   # leading dimensions not multiples of 16
+    (dict(A=4096 + 8), -2), (dict(B=8192 + 8), -2),   # rows not 16-byte aligned
+    (dict(c=0), -2),                          # no model for fp8 operands
+    (dict(tile=1), -2), (dict(tile=2), -2), (dict(tile=3), -2),
+    (dict(c=2, K=256, lda=256, ws=1 << 20, wsb=2 * 64 * 64 * 4 - 1), -3),
+])
+def test_f8_invalid_arguments_rejected_before_any_launch(sg, kw, code):
+    assert call_f8(sg, **kw) == code
+    assert sg.last_error() != ""
+
+
+def test_f8_empty_output_is_a_noop(sg):
+    assert call_f8(sg, M=0, C=None, A=None) == 0
+    assert call_f8(sg, N=0, C=None, B=None) == 0
