@@ -151,9 +151,11 @@ int sfc_gemm_ex(int64_t M, int64_t N, int64_t K,
  * ceil(K/128)) layers, whose workspace sfc_gemm_ws_size(M, N, K, c) bounds.
  * Restrictions (else SFC_ERR_UNSUPPORTED, nothing enqueued): A and B 16-byte
  * aligned, lda, ldb, K and N multiples of 16; tile SFC_TILE_AUTO or
- * SFC_TILE_256x256 (256x256 blocks); ca_layers >= 1 (SFC_CA_AUTO is not
- * offered: the model is calibrated for bf16).  Other arguments and errors as
- * for sfc_gemm_ex.
+ * SFC_TILE_256x256 (256x256 blocks).  ca_layers = SFC_CA_AUTO picks the layer
+ * count with the model of sfc_gemm_model for 256x256 blocks, evaluated on the
+ * bf16 problem with the same number of K blocks (K' = 64*ceil(K/128)): a
+ * 128-deep fp8 block moves the bytes of a 64-deep bf16 block and takes the same
+ * MFMA time.  Other arguments and errors as for sfc_gemm_ex.
  */
 int sfc_gemm_f8_ex(int64_t M, int64_t N, int64_t K,
                    const void *A, int64_t lda,

@@ -120,8 +120,6 @@ inline Checked check_gemm_f8_args(int64_t M, int64_t N, int64_t K, const void* A
   Checked c = check_gemm_args(M, N, K, A, lda, B, ldb, C, ldc, out_type, ca_layers, tile, order, sched, ws,
                               ws_bytes);
   if (c.code != SFC_OK || M == 0 || N == 0) return c;
-  if (ca_layers == 0)
-    return fail(SFC_ERR_UNSUPPORTED, "fp8 operands need an explicit ca_layers (the model is calibrated for bf16)");
   if (tile != SFC_TILE_AUTO && tile != SFC_TILE_256x256)
     return fail(SFC_ERR_UNSUPPORTED, "fp8 operands run on 256x256 blocks");
   if (K > 0 && !f8_loads_ok(A, lda, B, ldb, K, N))

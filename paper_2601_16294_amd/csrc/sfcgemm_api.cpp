@@ -111,10 +111,21 @@ int make_plan(DeviceState& st, int64_t M, int64_t N, int64_t K, const void* A, i
   int rc = SFC_OK;
   if (f8) {
     // fp8 operands (checked by check_gemm_f8_args): 256x256 blocks, 128-deep K
-    // blocks, the given layer count
+    // blocks.  A 128-deep fp8 block moves the bytes of a 64-deep bf16 block and
+    // takes the same MFMA time, so SFC_CA_AUTO asks the model about the bf16
+    // problem with the same number of blocks.
     pl->vec = true;
     pl->tile = sfc::kT256x256;
-    pl->ce = sfc::effective_layers(K, ca_layers, 128);
+    int layers = ca_layers;
+    if (ca_layers == SFC_CA_AUTO) {
+      int occ[sfc::kNumTiles];
+      for (int t = 0; t < sfc::kNumTiles; ++t) occ[t] = 1;
+      rc = get_occupancy(st, sfc::kT256x256, ob, true, &occ[sfc::kT256x256], true);
+      if (rc != SFC_OK) return rc;
+      const int64_t k_equiv = (K > 0 ? sfc::ceil_div(K, 128) : 0) * sfc::kBK;
+      layers = sfc::model_choose(M, N, k_equiv, ob ? 2 : 4, st.num_cus, occ, sfc::kT256x256, SFC_CA_AUTO).layers;
+    }
+    pl->ce = sfc::effective_layers(K, layers, 128);
     pl->bm = pl->bn = 256;
     pl->gm = (int)sfc::ceil_div(M, 256);
     pl->gn = (int)sfc::ceil_div(N, 256);

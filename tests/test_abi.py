@@ -142,7 +142,6 @@ def call_f8(sg, **kw):
     (dict(N=40, ldb=64, ldc=64), -2),         # N not a multiple of 16
     (dict(lda=72), -2), (dict(ldb=72), -2),   # leading dimensions not multiples of 16
     (dict(A=4096 + 8), -2), (dict(B=8192 + 8), -2),   # rows not 16-byte aligned
-    (dict(c=0), -2),                          # no model for fp8 operands
     (dict(tile=1), -2), (dict(tile=2), -2), (dict(tile=3), -2),
     (dict(c=2, K=256, lda=256, ws=1 << 20, wsb=2 * 64 * 64 * 4 - 1), -3),
 ])

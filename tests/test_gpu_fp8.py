@@ -93,9 +93,6 @@ def test_unsupported_arguments_are_rejected():
         sg().sfc_gemm_f8_ex(A[:, :40], B[:40, :], C)          # K not a multiple of 16
     assert e.value.code == sg().SFC_ERR_UNSUPPORTED
     with pytest.raises(sg().SfcError) as e:
-        sg().sfc_gemm_f8_ex(A, B, C, ca_layers=0)            # no model for fp8
-    assert e.value.code == sg().SFC_ERR_UNSUPPORTED
-    with pytest.raises(sg().SfcError) as e:
         sg().sfc_gemm_f8_ex(A, B, C, tile="128x128")
     assert e.value.code == sg().SFC_ERR_UNSUPPORTED
     torch.cuda.synchronize()
@@ -116,3 +113,20 @@ def test_full_size_8192_sampled():
     for r in (0, 4095, 8191):
         Cr, Rr = ogemm.gemm_ref_rows(Ab, Bb, N, K, K, N, row0=r, nrows=1)
         ocheck.assert_gemm_close(C[r:r + 1], Cr, Rr, f"fp8 8192^3 row {r}")
+
+
+@pytest.mark.parametrize("M,N,K", [(1024, 1024, 16384), (512, 768, 4096), (300, 272, 1040)])
+def test_auto_layers(M, N, K):
+    """SFC_CA_AUTO on fp8 operands: the model's layer count for the equivalent
+    bf16 problem (K' = 64*ceil(K/128), 256x256 blocks); the result meets the
+    bar whatever the count."""
+    A = draw_e4m3(M, K, ("normal", 0.0, 0.1), 71 + M)
+    B = draw_e4m3(K, N, ("normal", 0.0, 0.1), 72 + N)
+    Cr, R = ref(A, B, M, N, K)
+    C = to_host(run8(A, B, M, N, K, "f32", c=0))
+    ocheck.assert_gemm_close(C, Cr, R, f"fp8 auto {M}x{N}x{K}")
+    # the count the model picks for the equivalent bf16 problem is a K-dominant
+    # choice with layers for the first shape
+    pick = sg().sfc_gemm_model(M, N, 64 * -(-K // 128), out="f32", tile="256x256")
+    if (M, N, K) == (1024, 1024, 16384):
+        assert pick["layers"] > 1
