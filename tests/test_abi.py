@@ -143,6 +143,7 @@ def call_f8(sg, **kw):
     (dict(lda=72), -2), (dict(ldb=72), -2),   # leading dimensions not multiples of 16
     (dict(A=4096 + 8), -2), (dict(B=8192 + 8), -2),   # rows not 16-byte aligned
     (dict(tile=1), -2), (dict(tile=2), -2), (dict(tile=3), -2),
+    (dict(lda=1 << 21), -2), (dict(ldb=1 << 23), -2),   # past the 32-bit per-lane offsets; no element path
     (dict(c=2, K=256, lda=256, ws=1 << 20, wsb=2 * 64 * 64 * 4 - 1), -3),
 ])
 def test_f8_invalid_arguments_rejected_before_any_launch(sg, kw, code):
