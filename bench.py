@@ -52,14 +52,14 @@ def log(msg: str) -> None:
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--reps", type=int, default=10, help="cold repetitions per workload")
     ap.add_argument("--no-workloads", action="store_true", help="headline only")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--order", default="hilbert", choices=["hilbert", "row_major"])
-    ap.add_argument("--sched", default="interleaved", choices=["interleaved", "block"])
+    ap.add_argument("--sched", default="interleaved", choices=["interleaved", "block", "interleaved_plain"])
     ap.add_argument("--only", default=None,
                     help="run the kernel of one workload (or fp8_square8192) K times and exit")
     ap.add_argument("--sweep", action="store_true", help="also run the 125-shape sweep")
@@ -176,8 +176,8 @@ def main():
     stream = torch.cuda.current_stream()
     W = {w.name: w for w in workloads()}
 
-    def run_once(dA, dB, C, w, c):
-        sg.sfc_gemm_ex(dA, dB, C, ca_layers=c, tile=w.tile, order=args.order, sched=args.sched,
+    def run_once(dA, dB, C, w, c, sched=None):
+        sg.sfc_gemm_ex(dA, dB, C, ca_layers=c, tile=w.tile, order=args.order, sched=sched or args.sched,
                        stream=stream)
 
     def prepare(g):
@@ -348,36 +348,45 @@ def main():
             for x in wl.gemms:
                 pm = sg.sfc_gemm_plan(x.M, x.N, x.K, 0, wl.tile)
                 entry["model_choice"].append({"tile": f"{pm['BM']}x{pm['BN']}", "ca_layers": pm["layers"]})
-            per_c = {}
-            for c in wl.ca_layers:
-                label = "auto" if c == 0 else c
+            def timed(c, sched=None):
                 cold_t = warm_t = 0.0
                 for gg in wl.gemms:
                     _, _, a, b, cc = prepare(gg)
                     for _ in range(3):
-                        run_once(a, b, cc, wl, c)
+                        run_once(a, b, cc, wl, c, sched)
                     torch.cuda.synchronize()
                     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
                           for _ in range(args.reps)]
                     for s, e in ev:                           # cold: caches flushed, untimed
                         flush.zero_()
                         s.record(stream)
-                        run_once(a, b, cc, wl, c)
+                        run_once(a, b, cc, wl, c, sched)
                         e.record(stream)
                     torch.cuda.synchronize()
                     cold_t += sum(s.elapsed_time(e) for s, e in ev) / args.reps
                     s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
                     s.record(stream)
                     for _ in range(args.reps):
-                        run_once(a, b, cc, wl, c)
+                        run_once(a, b, cc, wl, c, sched)
                     e.record(stream)
                     torch.cuda.synchronize()
                     warm_t += s.elapsed_time(e) / args.reps
                     del a, b, cc
-                per_c[label] = {"cold_ms": round(cold_t, 4), "warm_ms": round(warm_t, 4),
-                                "tflops_cold": round(wl.flops / (cold_t * 1e-3) / 1e12, 2),
-                                "tflops_warm": round(wl.flops / (warm_t * 1e-3) / 1e12, 2)}
+                return {"cold_ms": round(cold_t, 4), "warm_ms": round(warm_t, 4),
+                        "tflops_cold": round(wl.flops / (cold_t * 1e-3) / 1e12, 2),
+                        "tflops_warm": round(wl.flops / (warm_t * 1e-3) / 1e12, 2)}
+
+            per_c = {}
+            for c in wl.ca_layers:
+                label = "auto" if c == 0 else c
+                per_c[label] = timed(c)
                 log(f"[bench] {name} c={label}: {per_c[label]}")
+            if len(wl.ca_layers) > 1:
+                # chiplet-aware placement of the layers against the hardware
+                # workgroup order, at the model's layer count
+                entry["layer_placement"] = {"chiplet_aware": per_c["auto"],
+                                            "hardware_order": timed(0, "interleaved_plain")}
+                log(f"[bench] {name} placement: {entry['layer_placement']}")
             best_c = max(per_c, key=lambda k: per_c[k]["tflops_cold"])
             best = per_c[best_c]
             entry.update({"per_ca_layers": per_c if len(per_c) > 1 else None, "best_ca_layers": best_c,

@@ -69,6 +69,9 @@ extern "C" {
                                     chiplet (XCD) owns a contiguous sub-segment of it */
 #define SFC_SCHED_BLOCK       1  /* workgroup r takes the r-th contiguous range of
                                     positions (the block partition of Section III.A) */
+#define SFC_SCHED_INTERLEAVED_PLAIN 2  /* as SFC_SCHED_INTERLEAVED with r = the
+                                    hardware workgroup index, so consecutive positions
+                                    go to different chiplets; for comparison only */
 
 /*
  * sfc_tile_order -- the block order of a gm x gn grid (Section II.B; the map

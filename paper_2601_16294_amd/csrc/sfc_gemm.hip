@@ -1249,7 +1249,8 @@ __global__ __launch_bounds__(NW * 64, 1) void sfc_gemm_kernel(GemmParams p) {
   if constexpr (VEC) read_offsets<BM, BN, NW, F8>(wm, wn, lane, lds_addr(smem) + (uint32_t)Ring<BM, BN, NW, F8>::B_OFF, ro);
 
   const int P = gridDim.x;
-  const int rank = xcd_rank(blockIdx.x, P);
+  // SFC_SCHED_INTERLEAVED_PLAIN keeps the hardware order (comparison only)
+  const int rank = p.sched == 2 ? (int)blockIdx.x : xcd_rank(blockIdx.x, P);
   // task counts are below 2^31 (the library checks it), so 32-bit indices do
   const int NT = (int)p.tasks;
   int t_begin, t_end, t_step;

@@ -56,7 +56,7 @@ inline Checked check_gemm_args(int64_t M, int64_t N, int64_t K, const void* A, i
   if (tile < SFC_TILE_AUTO || tile > SFC_TILE_256x256) return fail(SFC_ERR_INVALID_ARG, "unknown tile");
   if (order != SFC_ORDER_HILBERT && order != SFC_ORDER_ROW_MAJOR)
     return fail(SFC_ERR_INVALID_ARG, "unknown order");
-  if (sched != SFC_SCHED_INTERLEAVED && sched != SFC_SCHED_BLOCK)
+  if (sched != SFC_SCHED_INTERLEAVED && sched != SFC_SCHED_BLOCK && sched != SFC_SCHED_INTERLEAVED_PLAIN)
     return fail(SFC_ERR_INVALID_ARG, "unknown sched");
   if (M == 0 || N == 0) return ok();   // nothing to write
   if (!C) return fail(SFC_ERR_INVALID_ARG, "C is NULL");

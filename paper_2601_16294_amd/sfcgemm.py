@@ -30,7 +30,7 @@ SFC_CA_AUTO = 0
 TILES = {"auto": 0, "128x128": 1, "256x128": 2, "128x256": 3, "256x256": 4}
 TILE_NAMES = {v: k for k, v in TILES.items()}
 ORDERS = {"hilbert": 0, "row_major": 1}
-SCHEDS = {"interleaved": 0, "block": 1}
+SCHEDS = {"interleaved": 0, "block": 1, "interleaved_plain": 2}
 
 # Every symbol include/sfcgemm.h declares.
 EXPORTS = ["sfc_tile_order", "sfc_tile_order_ex", "sfc_gemm", "sfc_gemm_bf16out", "sfc_gemm_ws_size",

@@ -124,7 +124,7 @@ def test_order_and_schedule_never_change_bits(tile):
     A, B = operands(M, N, K, 700)
     ref = run_gemm(A, B, M, N, K, tile=tile)
     for order in ("hilbert", "row_major"):
-        for sched in ("interleaved", "block"):
+        for sched in ("interleaved", "block", "interleaved_plain"):
             assert np.array_equal(run_gemm(A, B, M, N, K, tile=tile, order=order, sched=sched), ref)
     assert np.array_equal(run_gemm(A, B, M, N, K, tile=tile), ref)   # run to run
 
