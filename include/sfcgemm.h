@@ -48,7 +48,14 @@ extern "C" {
 #define SFC_OUT_BF16 1           /* C holds bf16, rounded to nearest even */
 
 /* ---- block (tile) shape BM x BN of the output grid --------------------- */
-#define SFC_TILE_AUTO    0       /* chosen from M, N, K and ca_layers */
+#define SFC_TILE_AUTO    0       /* chosen from M, N, K and ca_layers.  With one
+                                    layer, 256-row blocks and a last round of
+                                    blocks at most half full, the last block columns
+                                    that make up that round are computed by a second
+                                    launch (same stream) with 128-row blocks of the
+                                    same width, which fill one round in about half
+                                    the time; result bits are those of the single
+                                    launch */
 #define SFC_TILE_128x128 1
 #define SFC_TILE_256x128 2       /* BM = 256, BN = 128 */
 #define SFC_TILE_128x256 3       /* BM = 128, BN = 256 */
@@ -170,7 +177,8 @@ int sfc_gemm_f8_ex(int64_t M, int64_t N, int64_t K,
 /*
  * sfc_gemm_plan -- what sfc_gemm_ex would launch, without launching
  * (fp32 output, 16-byte aligned operands).  ca_layers may be SFC_CA_AUTO and
- * tile SFC_TILE_AUTO; the plan then shows the model's choice.
+ * tile SFC_TILE_AUTO; the plan then shows the model's choice (for the whole
+ * grid: a half-height strip that SFC_TILE_AUTO may add is not shown).
  *   plan[0] = BM, plan[1] = BN, plan[2] = gm, plan[3] = gn, plan[4] = c_eff,
  *   plan[5] = number of persistent workgroups, plan[6] = workgroups per CU.
  * Needs a device (it queries the CU count and kernel occupancy).

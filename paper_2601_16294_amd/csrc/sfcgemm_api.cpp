@@ -170,6 +170,80 @@ int make_plan(DeviceState& st, int64_t M, int64_t N, int64_t K, const void* A, i
   return SFC_OK;
 }
 
+// Wave quantisation of the last round.  With T = gm*gn blocks and S resident
+// workgroups the last of ceil(T/S) rounds holds r = T mod S blocks.  When r <= S/2
+// and a kernel with half-height blocks of the same width exists, the last
+// w = ceil(r/gm) block columns go to a second launch with half-height blocks: their
+// 2*gm*w <= S blocks form one round that takes about half as long, and the first
+// launch keeps at most floor(T/S) full rounds.  Every element is still one full
+// ascending K pass of the same MFMA sequence, so no result bit changes.
+struct Split {
+  bool on = false;
+  int w = 0;      // block columns moved to the strip
+  Plan strip;     // the strip's plan (half-height blocks)
+};
+
+int plan_tail_split(DeviceState& st, const Plan& pl, int64_t M, int64_t N, int64_t K, const void* A,
+                    int64_t lda, const void* B, int64_t ldb, bool ob, Split* sp) {
+  sp->on = false;
+  if (pl.ce != 1 || !pl.vec) return SFC_OK;
+  int half;
+  if (pl.tile == sfc::kT256x256) half = sfc::kT128x256;
+  else if (pl.tile == sfc::kT256x128) half = sfc::kT128x128;
+  else return SFC_OK;
+  const int64_t T = (int64_t)pl.gm * pl.gn;
+  const int64_t S = (int64_t)st.num_cus * pl.occ;
+  const int64_t r = T % S;
+  if (T <= S || r == 0 || 2 * r > S) return SFC_OK;
+  const int w = (int)sfc::ceil_div(r, pl.gm);
+  if (w >= pl.gn) return SFC_OK;
+  int occ2 = 1;
+  int rc = get_occupancy(st, half, ob, true, &occ2);
+  if (rc != SFC_OK) return rc;
+  Plan& q = sp->strip;
+  q.tile = half;
+  q.bm = sfc::tile_bm(half);
+  q.bn = sfc::tile_bn(half);
+  const int64_t n1 = (int64_t)(pl.gn - w) * pl.bn;
+  q.gm = (int)sfc::ceil_div(M, q.bm);
+  q.gn = (int)sfc::ceil_div(N - n1, q.bn);
+  q.ce = 1;
+  q.nk = pl.nk;
+  q.occ = occ2;
+  q.vec = sfc::vector_loads_ok(A, lda, static_cast<const uint16_t*>(B) + n1, ldb, K, N - n1);
+  const int64_t tasks = (int64_t)q.gm * q.gn;
+  if (!q.vec || tasks > (int64_t)st.num_cus * occ2) return SFC_OK;
+  q.grid = (int)tasks;
+  sp->w = w;
+  sp->on = true;
+  return SFC_OK;
+}
+
+// One GEMM launch of plan pl into out (C, or the layer copies when pl.ce > 1).
+// Must be called with g_mu held.
+int launch_plan(DeviceState& st, const Plan& pl, int64_t M, int64_t N, int64_t K, const void* A, int64_t lda,
+                const void* B, int64_t ldb, void* out, int64_t ldo, int64_t layer_stride, bool out_bf16,
+                int order, int sched, hipStream_t stream, bool f8) {
+  const int32_t* table = nullptr;
+  int rc = get_table(st, pl.gm, pl.gn, order, stream, &table);
+  if (rc != SFC_OK) return rc;
+  sfc::GemmParams p;
+  p.M = M; p.N = N; p.K = K;
+  p.A = reinterpret_cast<const uint16_t*>(A); p.lda = lda;
+  p.B = reinterpret_cast<const uint16_t*>(B); p.ldb = ldb;
+  p.out = out; p.ldo = ldo; p.out_layer_stride = layer_stride;
+  p.table = table;
+  p.gm = pl.gm; p.gn = pl.gn;
+  p.layers = pl.ce;
+  p.nk = pl.nk;
+  p.tasks = (int64_t)pl.gm * pl.gn * pl.ce;
+  p.sched = sched;
+  p.pad_ = 0;
+  hipError_t e = sfc::launch_gemm(pl.tile, out_bf16, pl.vec, p, pl.grid, stream, f8);
+  if (e != hipSuccess) return hip_fail(e, "GEMM launch");
+  return SFC_OK;
+}
+
 int gemm_impl(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* B,
               int64_t ldb, void* C, int64_t ldc, int out_type, int ca_layers, int tile, int order,
               int sched, void* ws, size_t ws_bytes, void* stream_ptr, bool f8 = false) {
@@ -190,9 +264,27 @@ int gemm_impl(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const
   Plan pl;
   rc = make_plan(*st, M, N, K, A, lda, B, ldb, ob, ca_layers, tile, &pl, f8);
   if (rc != SFC_OK) return rc;
-  const int32_t* table = nullptr;
-  rc = get_table(*st, pl.gm, pl.gn, order, stream, &table);
-  if (rc != SFC_OK) return rc;
+
+  // the block shape is the library's to choose: a half-height strip may take
+  // a partial last round
+  Split sp;
+  if (tile == SFC_TILE_AUTO && !f8) {
+    rc = plan_tail_split(*st, pl, M, N, K, A, lda, B, ldb, ob, &sp);
+    if (rc != SFC_OK) return rc;
+  }
+  if (sp.on) {
+    Plan main = pl;
+    main.gn -= sp.w;
+    const int64_t tasks = (int64_t)main.gm * main.gn;
+    const int64_t slots = (int64_t)st->num_cus * main.occ;
+    main.grid = (int)(tasks < slots ? tasks : slots);
+    const int64_t n1 = (int64_t)main.gn * main.bn;
+    rc = launch_plan(*st, main, M, n1, K, A, lda, B, ldb, C, ldc, 0, ob, order, sched, stream, false);
+    if (rc != SFC_OK) return rc;
+    const size_t esz = ob ? 2 : 4;
+    return launch_plan(*st, sp.strip, M, N - n1, K, A, lda, static_cast<const uint16_t*>(B) + n1, ldb,
+                       static_cast<char*>(C) + (size_t)n1 * esz, ldc, 0, ob, order, sched, stream, false);
+  }
 
   float* W = nullptr;
   if (pl.ce > 1) {
@@ -217,23 +309,11 @@ int gemm_impl(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const
     }
   }
 
-  sfc::GemmParams p;
-  p.M = M; p.N = N; p.K = K;
-  p.A = reinterpret_cast<const uint16_t*>(A); p.lda = lda;
-  p.B = reinterpret_cast<const uint16_t*>(B); p.ldb = ldb;
-  if (pl.ce > 1) { p.out = W; p.ldo = N; p.out_layer_stride = M * N; }
-  else { p.out = C; p.ldo = ldc; p.out_layer_stride = 0; }
-  p.table = table;
-  p.gm = pl.gm; p.gn = pl.gn;
-  p.layers = pl.ce;
-  p.nk = pl.nk;
-  p.tasks = (int64_t)pl.gm * pl.gn * pl.ce;
-  p.sched = sched;
-  p.pad_ = 0;
-  hipError_t e = sfc::launch_gemm(pl.tile, ob && pl.ce == 1, pl.vec, p, pl.grid, stream, f8);
-  if (e != hipSuccess) return hip_fail(e, "GEMM launch");
+  if (pl.ce > 1) rc = launch_plan(*st, pl, M, N, K, A, lda, B, ldb, W, N, M * N, false, order, sched, stream, f8);
+  else rc = launch_plan(*st, pl, M, N, K, A, lda, B, ldb, C, ldc, 0, ob, order, sched, stream, f8);
+  if (rc != SFC_OK) return rc;
   if (pl.ce > 1) {
-    e = sfc::launch_reduce(W, pl.ce, M, N, C, ldc, ob, stream);
+    hipError_t e = sfc::launch_reduce(W, pl.ce, M, N, C, ldc, ob, stream);
     if (e != hipSuccess) return hip_fail(e, "reduction launch");
   }
   return SFC_OK;
