@@ -320,8 +320,24 @@ def main():
         del fa, fb
     except (RuntimeError, TypeError) as e:   # not offered by this torch build / device
         fp8["library_same_workload"] = {"unavailable": str(e)[:120]}
+    # the same shape with OCP E5M2 operands (sfc_gemm_f8_fmt_ex)
+    from paper_2601_16294_amd.inputs import draw_fp8
+    a5 = sg.to_device_u8(draw_fp8(g.M, g.K, ("normal", 0.0, 1.0), 2101, fmt="e5m2"))
+    b5 = sg.to_device_u8(draw_fp8(g.K, g.N, ("normal", 0.0, 1.0), 2102, fmt="e5m2"))
+    for _ in range(args.warmup):
+        sg.sfc_gemm_f8_ex(a5, b5, c8, stream=stream, a_format="e5m2", b_format="e5m2")
+    torch.cuda.synchronize()
+    ev5 = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    for s0, s1 in ev5:
+        s0.record(stream)
+        sg.sfc_gemm_f8_ex(a5, b5, c8, stream=stream, a_format="e5m2", b_format="e5m2")
+        s1.record(stream)
+    torch.cuda.synchronize()
+    f5_ms = sum(x.elapsed_time(y) for x, y in ev5) / args.steps
+    fp8["e5m2"] = {"call": "sfc_gemm_f8_fmt_ex, E5M2 A and B ~ N(0,1), bf16 out", "ms": round(f5_ms, 4),
+                   "tflops": round(g.flops / (f5_ms * 1e-3) / 1e12, 1)}
     log(f"[bench] fp8 {fp8}")
-    del a8, b8, c8
+    del a8, b8, c8, a5, b5
     torch.cuda.empty_cache()
 
     # ---------------------------------------------- sustained MFMA throughput
@@ -410,7 +426,7 @@ def main():
     if not args.no_cpu_baseline:
         from oracle import gemm as ogemm
         threads = ogemm.threads()
-        rows = 8
+        rows = 4 * threads                 # every thread busy while calibrating
         t = time.perf_counter()
         ogemm.gemm_ref_rows(A_host, B_host, g.N, g.K, g.K, g.N, row0=0, nrows=rows)
         dt = time.perf_counter() - t

@@ -174,6 +174,27 @@ int sfc_gemm_f8_ex(int64_t M, int64_t N, int64_t K,
                    int out_type, int ca_layers, int tile, int order, int sched,
                    void *ws, size_t ws_bytes, void *stream);
 
+/* ---- 8-bit float formats --------------------------------------------------- */
+#define SFC_FP8_E4M3 0   /* OCP E4M3: bias 7, 3 mantissa bits, no infinities, 0x7F/0xFF NaN */
+#define SFC_FP8_E5M2 1   /* OCP E5M2: bias 15, 2 mantissa bits, 0x7C/0xFC = +-inf,
+                            0x7D-0x7F/0xFD-0xFF NaN (the IEEE-style 8-bit format) */
+
+/*
+ * sfc_gemm_f8_fmt_ex -- sfc_gemm_f8_ex with the format of each operand chosen:
+ * a_format and b_format are SFC_FP8_E4M3 or SFC_FP8_E5M2 (the two 8-bit float
+ * formats of the same matrix instruction; mixed pairs allowed).  Every value of
+ * either format is a bf16 value, so products are exact in fp32 as for E4M3.
+ * Errors: SFC_ERR_INVALID_ARG for another format code, else as sfc_gemm_f8_ex.
+ * sfc_gemm_f8_ex is this call with both formats SFC_FP8_E4M3.
+ */
+int sfc_gemm_f8_fmt_ex(int64_t M, int64_t N, int64_t K,
+                       const void *A, int64_t lda,
+                       const void *B, int64_t ldb,
+                       void *C, int64_t ldc,
+                       int out_type, int a_format, int b_format,
+                       int ca_layers, int tile, int order, int sched,
+                       void *ws, size_t ws_bytes, void *stream);
+
 /*
  * sfc_gemm_plan -- what sfc_gemm_ex would launch, without launching
  * (fp32 output, 16-byte aligned operands).  ca_layers may be SFC_CA_AUTO and

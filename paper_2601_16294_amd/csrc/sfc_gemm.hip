@@ -40,7 +40,8 @@
 //   * bf16 output: v_permlane16_swap pairs two fragments so that every lane
 //     stores 8 consecutive columns (16 bytes); a store instruction costs about
 //     the same whatever its width, so this halves the epilogue.
-//   * fp8 operands (F8): the rings hold the same bytes (an A block row is 128
+//   * fp8 operands (F8 = 1 + a + 2b with a, b the OCP formats of A and B, 0 for
+//     E4M3 and 1 for E5M2; F8 = 0 for bf16): the rings hold the same bytes (an A block row is 128
 //     fp8, a B stage 64 rows of BN fp8); each 64-deep step is MFMA 32x32x64
 //     f8f6f4 per 32x32 fragment, fed by two 16-byte A reads and four
 //     ds_read_b64_tr_b8 B reads per fragment, and the 32x32 accumulators are
@@ -154,7 +155,7 @@ __device__ __forceinline__ void wait_lds_all() { asm volatile("s_waitcnt lgkmcnt
 // loads and waits).  A wave's fragment reads per 32-deep step are FM b128
 // reads of A and 2*FN transposing reads of B, so the grid keeps the wave
 // sub-block at most twice as wide as tall.
-template <int BM, int BN, int NW, bool F8>
+template <int BM, int BN, int NW, int F8>
 struct Tile {
   static_assert(NW == 4 || NW == 8, "4 or 8 waves");
   static constexpr int THREADS = NW * 64;
@@ -173,16 +174,16 @@ struct Tile {
 };
 
 // One accumulator fragment: 16x16 fp32 (4 per lane) or 32x32 fp32 (16 per lane).
-template <bool F8>
-using AccFrag = typename std::conditional<F8, f32x16, f32x4>::type;
-template <int BM, int BN, int NW, bool F8>
+template <int F8>
+using AccFrag = typename std::conditional<(F8 != 0), f32x16, f32x4>::type;
+template <int BM, int BN, int NW, int F8>
 using Acc = AccFrag<F8>[Tile<BM, BN, NW, F8>::FM][Tile<BM, BN, NW, F8>::FN];
 
 // Operand fragments of one step: 8 bf16 per lane (16x32), or 32 fp8 bytes per
 // lane (32x64).
-template <bool F8>
-using OpFrag = typename std::conditional<F8, i32x8, bf16x8>::type;
-template <int BM, int BN, int NW, bool F8>
+template <int F8>
+using OpFrag = typename std::conditional<(F8 != 0), i32x8, bf16x8>::type;
+template <int BM, int BN, int NW, int F8>
 struct Frags {
   OpFrag<F8> a[Tile<BM, BN, NW, F8>::FM];
   OpFrag<F8> b[Tile<BM, BN, NW, F8>::FN];
@@ -218,7 +219,7 @@ __device__ __forceinline__ bf16x8 read_b_pair(const uint16_t* p, int half_stride
 
 // All operand fragments of one 32-deep step from an A block [BM][64] (step
 // ks) and a B buffer [..][BN] (rows kbase .. kbase+31).
-template <int BM, int BN, int NW, bool F8>
+template <int BM, int BN, int NW, int F8>
 __device__ __forceinline__ void load_frags(const uint16_t* As, const uint16_t* Bs, int wm, int wn,
                                            int lane, int ks, int kbase, Frags<BM, BN, NW, F8>& f) {
   using T = Tile<BM, BN, NW, F8>;
@@ -230,7 +231,7 @@ __device__ __forceinline__ void load_frags(const uint16_t* As, const uint16_t* B
 }
 
 // acc += one 32-deep step.
-template <int BM, int BN, int NW, bool F8>
+template <int BM, int BN, int NW, int F8>
 __device__ __forceinline__ void mma_step(const Frags<BM, BN, NW, F8>& cur, Acc<BM, BN, NW, F8>& acc) {
   using T = Tile<BM, BN, NW, F8>;
 #pragma unroll
@@ -262,9 +263,9 @@ constexpr int kBias = 4096;    // bytes; keeps every biased voffset positive
 // bytes (64 bf16 or 128 fp8 elements of K), a B stage is 64*BN bytes (32 rows
 // of BN bf16 or 64 rows of BN fp8).  K depth, in elements, of a block and of a
 // B stage:
-template <bool F8>
+template <int F8>
 constexpr int block_k() { return F8 ? 128 : kBK; }
-template <bool F8>
+template <int F8>
 constexpr int stage_k() { return F8 ? 64 : kSK; }
 // fp8 B stages: chunk c (16 columns) of row k is stored at chunk c ^ (2*(k&7));
 // a transposing read of 8 consecutive rows at two adjacent chunks (2m, 2m+1)
@@ -274,7 +275,7 @@ __device__ __forceinline__ int b_swz8(int k) { return (k & 7) << 1; }
 // The loads of block b+D are issued during block b (prefetch depth D): the A
 // ring has D+1 block slots, the B ring 2D stage slots.  D = 3 where the LDS
 // holds that at the same occupancy (128x256: exactly 160 KiB), else 2.
-template <int BM, int BN, int NW, bool F8>
+template <int BM, int BN, int NW, int F8>
 struct Ring {
   static constexpr int A_BLK = BM * kBK;                 // elements of one A block
   static constexpr int B_STG = kSK * BN;                 // elements of one B stage
@@ -320,20 +321,20 @@ __device__ __forceinline__ i32x4 make_rsrc_addr(uint64_t a, uint32_t num_records
 }
 
 // Per-lane, per-task load offsets (bytes, biased).
-template <int BM, int BN, int NW, bool F8>
+template <int BM, int BN, int NW, int F8>
 struct RingLanes {
   int a_voff[Ring<BM, BN, NW, F8>::APB];
   int b_voff[Ring<BM, BN, NW, F8>::BPW];
 };
 
 // K index (within a block, in elements) at which A load j of this lane starts.
-template <bool F8>
+template <int F8>
 __device__ __forceinline__ int a_load_k(int wave, int apb, int j, int lane) {
   const int row = (wave * apb + j) * 8 + (lane >> 3);
   return ((lane & 7) ^ ((row >> 1) & 7)) * (F8 ? 16 : 8);
 }
 
-template <int BM, int BN, int NW, bool F8>
+template <int BM, int BN, int NW, int F8>
 __device__ __forceinline__ void ring_lanes(const GemmParams& p, int64_t m0, int64_t n0, int wave,
                                            int lane, RingLanes<BM, BN, NW, F8>& L) {
   using R = Ring<BM, BN, NW, F8>;
@@ -341,14 +342,14 @@ __device__ __forceinline__ void ring_lanes(const GemmParams& p, int64_t m0, int6
   for (int j = 0; j < R::APB; ++j) {
     const int row = (wave * R::APB + j) * 8 + (lane >> 3);
     const int c = (lane & 7) ^ ((row >> 1) & 7);
-    if constexpr (F8)
+    if constexpr (F8 != 0)
       L.a_voff[j] = (m0 + row < p.M) ? (int)(row * p.lda + c * 16) + kBias - (j & 3) * 1024 : kOobOffset;
     else
       L.a_voff[j] = (m0 + row < p.M) ? (int)((row * p.lda + c * 8) * 2) + kBias - (j & 3) * 1024 : kOobOffset;
   }
 #pragma unroll
   for (int j = 0; j < R::BPW; ++j) {
-    if constexpr (F8) {
+    if constexpr (F8 != 0) {
       const int eb = (wave * R::BPW + j) * 1024 + lane * 16;   // byte offset in the [64][BN] stage
       const int k = eb / BN;
       const int c = ((eb % BN) >> 4) ^ b_swz8(k);
@@ -364,7 +365,7 @@ __device__ __forceinline__ void ring_lanes(const GemmParams& p, int64_t m0, int6
 
 // Turn the A lanes whose load starts at a K index >= kin (within the block)
 // into out-of-range lanes, for the loads of a block that runs past K.
-template <int BM, int BN, int NW, bool F8>
+template <int BM, int BN, int NW, int F8>
 __device__ __forceinline__ void mask_a_lanes(RingLanes<BM, BN, NW, F8>& L, int wave, int lane, int64_t kin) {
   using R = Ring<BM, BN, NW, F8>;
 #pragma unroll
@@ -373,7 +374,7 @@ __device__ __forceinline__ void mask_a_lanes(RingLanes<BM, BN, NW, F8>& L, int w
 }
 
 // The same without a branch: masks only when `on` (wave-uniform).
-template <int BM, int BN, int NW, bool F8>
+template <int BM, int BN, int NW, int F8>
 __device__ __forceinline__ void mask_a_lanes_if(RingLanes<BM, BN, NW, F8>& L, int wave, int lane, int64_t kin, bool on) {
   using R = Ring<BM, BN, NW, F8>;
 #pragma unroll
@@ -388,17 +389,17 @@ __device__ __forceinline__ void mask_a_lanes_if(RingLanes<BM, BN, NW, F8>& L, in
 // fp8: A fragment i of step ks is two 16-byte reads, at a_rd[ks] + i*4096 and
 // a_d further (the next chunk, +-16 bytes under the swizzle); B fragment j is
 // four transposing reads of 8 rows, at b_rd[j] + q*8*BN.
-template <int BM, int BN, int NW, bool F8>
+template <int BM, int BN, int NW, int F8>
 struct ReadOffsets {
   uint32_t a_rd[2];
   uint32_t a_d;
   uint32_t b_rd[Tile<BM, BN, NW, F8>::FN];
 };
 
-template <int BM, int BN, int NW, bool F8>
+template <int BM, int BN, int NW, int F8>
 __device__ __forceinline__ void read_offsets(int wm, int wn, int lane, uint32_t b_ring, ReadOffsets<BM, BN, NW, F8>& o) {
   using T = Tile<BM, BN, NW, F8>;
-  if constexpr (F8) {
+  if constexpr (F8 != 0) {
     // A: lane l holds row l%32 of the fragment and K bytes 32*(l/32) .. +31 of
     // the 64-deep step, i.e. chunks 4ks + 2h and 4ks + 2h + 1 (h = l/32)
     const int row = wm * T::WTM + (lane & 31), h = lane >> 5;
@@ -447,11 +448,11 @@ __device__ __forceinline__ void read_b8(uint32_t addr, int q, i32x8& f) {
 
 // Read item t of a step, in the order the next step's MFMAs consume them:
 // A0, B0, B1, .., B(FN-1), A1, .., A(FM-1).
-template <int BM, int BN, int NW, bool F8>
+template <int BM, int BN, int NW, int F8>
 __device__ __forceinline__ void read_item(int t, uint32_t a_base, uint32_t a_d, uint32_t b_slot, const uint32_t* b_rd,
                                           Frags<BM, BN, NW, F8>& f) {
   using T = Tile<BM, BN, NW, F8>;
-  if constexpr (F8) {
+  if constexpr (F8 != 0) {
     if (t == 0 || t > T::FN) {
       const int i = t == 0 ? 0 : t - T::FN;
       read_a8(a_base, a_d, i, 0, f.a[i]);
@@ -486,7 +487,7 @@ struct SlotDma {
 };
 
 // Load pair q (loads 2q, 2q+1) of an A block (OP 1) or a B stage (OP 2).
-template <int BM, int BN, int NW, bool F8, int OP, int Q>
+template <int BM, int BN, int NW, int F8, int OP, int Q>
 __device__ __forceinline__ void dma_pair(const SlotDma& d, const RingLanes<BM, BN, NW, F8>& L) {
   constexpr int j = 2 * Q;
   if constexpr (OP == 1)
@@ -496,7 +497,7 @@ __device__ __forceinline__ void dma_pair(const SlotDma& d, const RingLanes<BM, B
 }
 
 // All loads of an A block (OP 1) or a B stage (OP 2).
-template <int BM, int BN, int NW, bool F8, int OP>
+template <int BM, int BN, int NW, int F8, int OP>
 __device__ __forceinline__ void dma_all(const SlotDma& d, const RingLanes<BM, BN, NW, F8>& L) {
   using R = Ring<BM, BN, NW, F8>;
   [&]<int... q>(std::integer_sequence<int, q...>) {
@@ -514,7 +515,7 @@ __device__ __forceinline__ void dma_all(const SlotDma& d, const RingLanes<BM, BN
 //   loads:  each load pair becomes three operations (set M0, load, load) in
 //           consecutive groups from evenly spaced starting groups, so that the
 //           MFMA between M0 and the first load covers the wait M0 needs.
-template <int BM, int BN, int NW, bool F8, int OP>
+template <int BM, int BN, int NW, int F8, int OP>
 struct StepPlan {
   using T = Tile<BM, BN, NW, F8>;
   static constexpr int G = T::FM * T::FN;
@@ -572,18 +573,18 @@ struct StepPlan {
 };
 
 // Per-step state of the split B reads: address and low half of each fragment.
-template <int BM, int BN, int NW, bool F8>
+template <int BM, int BN, int NW, int F8>
 struct BReads {
   uint32_t addr[Tile<BM, BN, NW, F8>::FN];
   i16x4 lo[Tile<BM, BN, NW, F8>::FN];
   uint32_t a_d;   // fp8: offset of the second half of an A fragment
 };
 
-template <int BM, int BN, int NW, bool F8, int OP, int r>
+template <int BM, int BN, int NW, int F8, int OP, int r>
 __device__ __forceinline__ void step_read(uint32_t a_base, uint32_t b_slot, const uint32_t* b_rd, BReads<BM, BN, NW, F8>& br,
                                           Frags<BM, BN, NW, F8>& nxt) {
   using T = Tile<BM, BN, NW, F8>;
-  if constexpr (F8) {
+  if constexpr (F8 != 0) {
     // A0 (halves 0, 1), B0 .. B(FN-1) (quarters 0..3 each), A1 .. A(FM-1)
     if constexpr (r < 2) {
       read_a8(a_base, br.a_d, 0, r, nxt.a[0]);
@@ -611,7 +612,7 @@ __device__ __forceinline__ void step_read(uint32_t a_base, uint32_t b_slot, cons
   }
 }
 
-template <int BM, int BN, int NW, bool F8, int OP, int g, int... r>
+template <int BM, int BN, int NW, int F8, int OP, int g, int... r>
 __device__ __forceinline__ void group_reads(uint32_t a_base, uint32_t b_slot, const uint32_t* b_rd,
                                             BReads<BM, BN, NW, F8>& br, Frags<BM, BN, NW, F8>& nxt, std::integer_sequence<int, r...>) {
   using P = StepPlan<BM, BN, NW, F8, OP>;
@@ -620,7 +621,7 @@ __device__ __forceinline__ void group_reads(uint32_t a_base, uint32_t b_slot, co
 
 // Load operation o of a step: o = 3q + k for load pair q (k 0: set M0, k 1
 // and 2: the pair's loads).
-template <int BM, int BN, int NW, bool F8, int OP, int o>
+template <int BM, int BN, int NW, int F8, int OP, int o>
 __device__ __forceinline__ void step_dma(const SlotDma& d0, const SlotDma& d1, const RingLanes<BM, BN, NW, F8>& L) {
   using P = StepPlan<BM, BN, NW, F8, OP>;
   constexpr int q = o / 3, k = o % 3;
@@ -639,14 +640,14 @@ __device__ __forceinline__ void step_dma(const SlotDma& d0, const SlotDma& d1, c
   }
 }
 
-template <int BM, int BN, int NW, bool F8, int OP, int g, int... o>
+template <int BM, int BN, int NW, int F8, int OP, int g, int... o>
 __device__ __forceinline__ void group_dma(const SlotDma& d0, const SlotDma& d1, const RingLanes<BM, BN, NW, F8>& L,
                                           std::integer_sequence<int, o...>) {
   using P = StepPlan<BM, BN, NW, F8, OP>;
   ((void)(P::dma_group(o) == g ? (step_dma<BM, BN, NW, F8, OP, o>(d0, d1, L), 0) : 0), ...);
 }
 
-template <int BM, int BN, int NW, bool F8, int OP, int g, typename X>
+template <int BM, int BN, int NW, int F8, int OP, int g, typename X>
 __device__ __forceinline__ void ring_group(Acc<BM, BN, NW, F8>& acc, const Frags<BM, BN, NW, F8>& cur, Frags<BM, BN, NW, F8>& nxt,
                                            uint32_t a_base, uint32_t b_slot, const uint32_t* b_rd,
                                            BReads<BM, BN, NW, F8>& br, const SlotDma& d0, const SlotDma& d1,
@@ -654,8 +655,9 @@ __device__ __forceinline__ void ring_group(Acc<BM, BN, NW, F8>& acc, const Frags
   using T = Tile<BM, BN, NW, F8>;
   using P = StepPlan<BM, BN, NW, F8, OP>;
   constexpr int i = g / T::FN, j = g % T::FN;
-  if constexpr (F8)   // fp8 E4M3 x E4M3 (formats 0, 0), unit scales (E8M0 127)
-    acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(cur.b[j], cur.a[i], acc[i][j], 0, 0, 0, 127, 0, 127);
+  if constexpr (F8 != 0)   // the first operand is B (format b), the second A (format a); unit scales (E8M0 127)
+    acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(cur.b[j], cur.a[i], acc[i][j], (F8 - 1) >> 1,
+                                                                (F8 - 1) & 1, 0, 127, 0, 127);
   else
     acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(cur.b[j], cur.a[i], acc[i][j], 0, 0, 0);
   if constexpr (OP == 2 && g == P::G0) {
@@ -674,7 +676,7 @@ __device__ __forceinline__ void ring_group(Acc<BM, BN, NW, F8>& acc, const Frags
   __builtin_amdgcn_sched_barrier(0);
 }
 
-template <int BM, int BN, int NW, bool F8, int OP, typename X, int... g>
+template <int BM, int BN, int NW, int F8, int OP, typename X, int... g>
 __device__ __forceinline__ void ring_groups(Acc<BM, BN, NW, F8>& acc, const Frags<BM, BN, NW, F8>& cur, Frags<BM, BN, NW, F8>& nxt,
                                             uint32_t a_base, uint32_t b_slot, const uint32_t* b_rd,
                                             BReads<BM, BN, NW, F8>& br, const SlotDma& d0, const SlotDma& d1,
@@ -688,7 +690,7 @@ __device__ __forceinline__ void ring_groups(Acc<BM, BN, NW, F8>& acc, const Frag
 // (ex.operator()<g>() runs in group g).  The groups are generated as
 // straight-line code (a loop this long is not always unrolled, and the
 // accumulators must stay in registers).
-template <int BM, int BN, int NW, bool F8, int OP, typename X>
+template <int BM, int BN, int NW, int F8, int OP, typename X>
 __device__ __forceinline__ void ring_step(Acc<BM, BN, NW, F8>& acc, const Frags<BM, BN, NW, F8>& cur, Frags<BM, BN, NW, F8>& nxt,
                                           uint32_t a_base, uint32_t b_slot, const ReadOffsets<BM, BN, NW, F8>& o,
                                           const SlotDma& d0, const SlotDma& d1, const RingLanes<BM, BN, NW, F8>& L,
@@ -742,7 +744,7 @@ __device__ __forceinline__ uint32_t b_stage_limit(const RingAddr& ra, int x) {
 // outside the B descriptors' ranges and read zeros; A block nb-1 is loaded with
 // its lanes past K masked (selects on the first groups of the step that issues
 // those loads, or in the prologue when nb <= D).
-template <int BM, int BN, int NW, bool F8>
+template <int BM, int BN, int NW, int F8>
 __device__ __forceinline__ void main_loop_ring(const RingAddr& ra, int nb, int64_t kin_last,
                                                const ReadOffsets<BM, BN, NW, F8>& o, RingLanes<BM, BN, NW, F8>& L, int lane,
                                                Acc<BM, BN, NW, F8>& acc) {
@@ -896,7 +898,7 @@ __device__ __forceinline__ void main_loop_ring(const RingAddr& ra, int nb, int64
 }
 
 // ---- main loop, general path: element loads staged in registers ---------------------------
-template <int BM, int BN, int NW, bool F8>
+template <int BM, int BN, int NW, int F8>
 __device__ __forceinline__ void main_loop_staged(const GemmParams& p, uint16_t* smem, int64_t m0,
                                                  int64_t n0, int kt0, int kt1, int tid, Acc<BM, BN, NW, F8>& acc) {
   using T = Tile<BM, BN, NW, F8>;
@@ -973,10 +975,10 @@ __device__ __forceinline__ u32x4 pair_to_row8(const f32x4& x, const f32x4& y) {
 // bf16 output, runs (g, g+1) are exchanged between the lane halves with
 // v_permlane32_swap so that each lane stores 8 consecutive columns (16 bytes).
 template <int BM, int BN, int NW, bool OUT_BF16>
-__device__ __forceinline__ void store_tile32(const GemmParams& p, const Acc<BM, BN, NW, true>& acc, int64_t m0,
+__device__ __forceinline__ void store_tile32(const GemmParams& p, const Acc<BM, BN, NW, 1>& acc, int64_t m0,
                                              int64_t n0, int64_t lstride, int wm, int wn, int lane, bool fast,
                                              bool fast16) {
-  using T = Tile<BM, BN, NW, true>;
+  using T = Tile<BM, BN, NW, 1>;
   typedef typename std::conditional<OUT_BF16, __bf16, float>::type OutT;
   OutT* out = reinterpret_cast<OutT*>(p.out) + lstride;
   const int h = lane >> 5;
@@ -1054,7 +1056,7 @@ __device__ __forceinline__ void store_tile32(const GemmParams& p, const Acc<BM, 
 // with 16-byte aligned rows only; a sub-block that does not fit the rings at
 // once goes in several row passes.  The caller synchronises the workgroup
 // before the rings are written again.
-template <int BM, int BN, int NW, bool F8, bool OUT_BF16>
+template <int BM, int BN, int NW, int F8, bool OUT_BF16>
 struct Staging {
   using T = Tile<BM, BN, NW, F8>;
   static constexpr int ES = OUT_BF16 ? 2 : 4;                 // bytes per output element
@@ -1083,7 +1085,7 @@ __device__ __forceinline__ u32x4 lds_read16(uint32_t addr) {
   return *(lds_u32x4c*)(uintptr_t)addr;
 }
 
-template <int BM, int BN, int NW, bool F8, bool OUT_BF16>
+template <int BM, int BN, int NW, int F8, bool OUT_BF16>
 __device__ __forceinline__ void store_tile_staged(const GemmParams& p, const Acc<BM, BN, NW, F8>& acc, int64_t m0,
                                                   int64_t n0, int64_t lstride, int wm, int wn, int wave, int lane,
                                                   uint32_t lds0) {
@@ -1097,7 +1099,7 @@ __device__ __forceinline__ void store_tile_staged(const GemmParams& p, const Acc
 #pragma unroll
   for (int pass = 0; pass < S::PASSES; ++pass) {
     // fragments of sub-block rows [pass*PASS_ROWS, +PASS_ROWS) into LDS
-    if constexpr (F8) {
+    if constexpr (F8 != 0) {
       // 32x32 fragments: lane l, run g: row 32i + l%32, columns 32j + 8g + 4(l/32)
       const int h = lane >> 5, r = lane & 31;
 #pragma unroll
@@ -1165,10 +1167,10 @@ __device__ __forceinline__ void store_tile_staged(const GemmParams& p, const Acc
   }
 }
 
-template <int BM, int BN, int NW, bool F8, bool OUT_BF16>
+template <int BM, int BN, int NW, int F8, bool OUT_BF16>
 __device__ __forceinline__ void store_tile(const GemmParams& p, const Acc<BM, BN, NW, F8>& acc, int64_t m0, int64_t n0,
                                            int64_t lstride, int wm, int wn, int lane, bool fast, bool fast16) {
-  if constexpr (F8) {
+  if constexpr (F8 != 0) {
     store_tile32<BM, BN, NW, OUT_BF16>(p, acc, m0, n0, lstride, wm, wn, lane, fast, fast16);
     return;
   } else {
@@ -1232,7 +1234,7 @@ __device__ __forceinline__ void store_tile(const GemmParams& p, const Acc<BM, BN
   }
 }
 
-template <int BM, int BN, int NW, bool F8, bool OUT_BF16, bool VEC>
+template <int BM, int BN, int NW, int F8, bool OUT_BF16, bool VEC>
 __global__ __launch_bounds__(NW * 64, 1) void sfc_gemm_kernel(GemmParams p) {
   using T = Tile<BM, BN, NW, F8>;
   static_assert(T::A_CH >= 1 && T::B_CH >= 1, "tile too small for the workgroup");
@@ -1290,7 +1292,7 @@ __global__ __launch_bounds__(NW * 64, 1) void sfc_gemm_kernel(GemmParams p) {
     for (int i = 0; i < T::FM; ++i)
 #pragma unroll
       for (int j = 0; j < T::FN; ++j) {
-        if constexpr (F8) acc[i][j] = f32x16{};
+        if constexpr (F8 != 0) acc[i][j] = f32x16{};
         else acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
       }
 
@@ -1350,21 +1352,30 @@ __global__ __launch_bounds__(NW * 64, 1) void sfc_gemm_kernel(GemmParams p) {
 static_assert(SFC_WAVES_256x256 == 4 || SFC_WAVES_256x256 == 8, "4 or 8 waves");
 static constexpr int fast_waves(int tile) { return tile == kT256x256 ? SFC_WAVES_256x256 : 4; }
 
-template <int BM, int BN, int NW, bool F8, bool OB, bool VEC>
+template <int BM, int BN, int NW, int F8, bool OB, bool VEC>
 static const void* kernel_ptr() {
   return reinterpret_cast<const void*>(&sfc_gemm_kernel<BM, BN, NW, F8, OB, VEC>);
 }
 
-// fp8 (OCP E4M3) operands: 256x256 blocks, fast path only.
-static const void* select_kernel_f8(int tile, bool ob) {
+// fp8 operands (f8 = 1 + a + 2b, a and b the formats of A and B: 0 OCP E4M3,
+// 1 OCP E5M2): 256x256 blocks, fast path only.
+static const void* select_kernel_f8(int tile, bool ob, int f8) {
   if (tile != kT256x256) return nullptr;
-  return ob ? kernel_ptr<256, 256, 4, true, true, true>() : kernel_ptr<256, 256, 4, true, false, true>();
+#define SFC_K8(F_) return ob ? kernel_ptr<256, 256, 4, F_, true, true>() : kernel_ptr<256, 256, 4, F_, false, true>()
+  switch (f8) {
+    case 1: SFC_K8(1);
+    case 2: SFC_K8(2);
+    case 3: SFC_K8(3);
+    case 4: SFC_K8(4);
+    default: return nullptr;
+  }
+#undef SFC_K8
 }
 
 static const void* select_kernel(int tile, bool ob, bool vec) {
 #define SFC_K(BM_, BN_, NW_)                                                                   \
-  return ob ? (vec ? kernel_ptr<BM_, BN_, NW_, false, true, true>() : kernel_ptr<BM_, BN_, 4, false, true, false>()) \
-            : (vec ? kernel_ptr<BM_, BN_, NW_, false, false, true>() : kernel_ptr<BM_, BN_, 4, false, false, false>())
+  return ob ? (vec ? kernel_ptr<BM_, BN_, NW_, 0, true, true>() : kernel_ptr<BM_, BN_, 4, 0, true, false>()) \
+            : (vec ? kernel_ptr<BM_, BN_, NW_, 0, false, true>() : kernel_ptr<BM_, BN_, 4, 0, false, false>())
   switch (tile) {
     case kT128x128: SFC_K(128, 128, 4);
     case kT256x128: SFC_K(256, 128, 4);
@@ -1378,16 +1389,16 @@ static const void* select_kernel(int tile, bool ob, bool vec) {
 static int threads_of(int tile, bool vec) { return (vec ? fast_waves(tile) : 4) * 64; }
 
 hipError_t launch_gemm(int tile, bool out_bf16, bool vec, const GemmParams& p, int grid,
-                       hipStream_t stream, bool f8) {
-  const void* k = f8 ? select_kernel_f8(tile, out_bf16) : select_kernel(tile, out_bf16, vec);
+                       hipStream_t stream, int f8) {
+  const void* k = f8 ? select_kernel_f8(tile, out_bf16, f8) : select_kernel(tile, out_bf16, vec);
   if (!k) return hipErrorInvalidValue;
   GemmParams local = p;
   void* args[] = {&local};
   return hipLaunchKernel(k, dim3(grid), dim3(threads_of(tile, vec)), args, 0, stream);
 }
 
-hipError_t gemm_occupancy(int tile, bool out_bf16, bool vec, int* blocks_per_cu, bool f8) {
-  const void* k = f8 ? select_kernel_f8(tile, out_bf16) : select_kernel(tile, out_bf16, vec);
+hipError_t gemm_occupancy(int tile, bool out_bf16, bool vec, int* blocks_per_cu, int f8) {
+  const void* k = f8 ? select_kernel_f8(tile, out_bf16, f8) : select_kernel(tile, out_bf16, vec);
   if (!k) return hipErrorInvalidValue;
   return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, k, threads_of(tile, vec), 0);
 }

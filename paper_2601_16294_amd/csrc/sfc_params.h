@@ -35,11 +35,12 @@ hipError_t launch_sfc_order(int gm, int gn, int order, int32_t* dev_out, hipStre
 
 // Persistent GEMM.  out_bf16 selects the epilogue; vec selects 128-bit loads
 // (needs 16-byte aligned A and B, lda, ldb, K and N multiples of 8).
-// f8: A and B hold OCP E4M3 bytes (lda, ldb in elements = bytes); 256x256 only.
+// f8 = 0: bf16 operands; f8 = 1 + a + 2b: A and B hold OCP fp8 bytes of format a
+// and b (0 E4M3, 1 E5M2; lda, ldb in elements = bytes); 256x256 only.
 hipError_t launch_gemm(int tile, bool out_bf16, bool vec, const GemmParams& p, int grid,
-                       hipStream_t stream, bool f8 = false);
+                       hipStream_t stream, int f8 = 0);
 // Workgroups of the given kernel variant that fit on one CU.
-hipError_t gemm_occupancy(int tile, bool out_bf16, bool vec, int* blocks_per_cu, bool f8 = false);
+hipError_t gemm_occupancy(int tile, bool out_bf16, bool vec, int* blocks_per_cu, int f8 = 0);
 
 // C[i][j] = sum_l W[l][i][j] (ascending l, fp32), W dense M x N per layer.
 hipError_t launch_reduce(const float* W, int layers, int64_t M, int64_t N, void* C, int64_t ldc,

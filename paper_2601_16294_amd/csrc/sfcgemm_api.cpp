@@ -79,8 +79,8 @@ int get_table(DeviceState& st, int gm, int gn, int order, hipStream_t stream, co
   return SFC_OK;
 }
 
-int get_occupancy(DeviceState& st, int tile, bool ob, bool vec, int* occ, bool f8 = false) {
-  int& o = st.occupancy[tile][ob][vec][f8];
+int get_occupancy(DeviceState& st, int tile, bool ob, bool vec, int* occ, int f8 = 0) {
+  int& o = st.occupancy[tile][ob][vec][f8 != 0];
   if (o == 0) {
     int v = 0;
     hipError_t e = sfc::gemm_occupancy(tile, ob, vec, &v, f8);
@@ -107,7 +107,7 @@ struct Plan {
 };
 
 int make_plan(DeviceState& st, int64_t M, int64_t N, int64_t K, const void* A, int64_t lda,
-              const void* B, int64_t ldb, bool ob, int ca_layers, int tile_api, Plan* pl, bool f8 = false) {
+              const void* B, int64_t ldb, bool ob, int ca_layers, int tile_api, Plan* pl, int f8 = 0) {
   int rc = SFC_OK;
   if (f8) {
     // fp8 operands (checked by check_gemm_f8_args): 256x256 blocks, 128-deep K
@@ -120,7 +120,7 @@ int make_plan(DeviceState& st, int64_t M, int64_t N, int64_t K, const void* A, i
     if (ca_layers == SFC_CA_AUTO) {
       int occ[sfc::kNumTiles];
       for (int t = 0; t < sfc::kNumTiles; ++t) occ[t] = 1;
-      rc = get_occupancy(st, sfc::kT256x256, ob, true, &occ[sfc::kT256x256], true);
+      rc = get_occupancy(st, sfc::kT256x256, ob, true, &occ[sfc::kT256x256], f8);
       if (rc != SFC_OK) return rc;
       const int64_t k_equiv = (K > 0 ? sfc::ceil_div(K, 128) : 0) * sfc::kBK;
       layers = sfc::model_choose(M, N, k_equiv, ob ? 2 : 4, st.num_cus, occ, sfc::kT256x256, SFC_CA_AUTO).layers;
@@ -130,7 +130,7 @@ int make_plan(DeviceState& st, int64_t M, int64_t N, int64_t K, const void* A, i
     pl->gm = (int)sfc::ceil_div(M, 256);
     pl->gn = (int)sfc::ceil_div(N, 256);
     pl->nk = (int)(K > 0 ? sfc::ceil_div(K, 128) : 0);
-    rc = get_occupancy(st, pl->tile, ob && pl->ce == 1, true, &pl->occ, true);
+    rc = get_occupancy(st, pl->tile, ob && pl->ce == 1, true, &pl->occ, f8);
     if (rc != SFC_OK) return rc;
     const int64_t tasks = (int64_t)pl->gm * pl->gn * pl->ce;
     const int64_t slots = (int64_t)st.num_cus * pl->occ;
@@ -223,7 +223,7 @@ int plan_tail_split(DeviceState& st, const Plan& pl, int64_t M, int64_t N, int64
 // Must be called with g_mu held.
 int launch_plan(DeviceState& st, const Plan& pl, int64_t M, int64_t N, int64_t K, const void* A, int64_t lda,
                 const void* B, int64_t ldb, void* out, int64_t ldo, int64_t layer_stride, bool out_bf16,
-                int order, int sched, hipStream_t stream, bool f8) {
+                int order, int sched, hipStream_t stream, int f8) {
   const int32_t* table = nullptr;
   int rc = get_table(st, pl.gm, pl.gn, order, stream, &table);
   if (rc != SFC_OK) return rc;
@@ -246,7 +246,7 @@ int launch_plan(DeviceState& st, const Plan& pl, int64_t M, int64_t N, int64_t K
 
 int gemm_impl(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* B,
               int64_t ldb, void* C, int64_t ldc, int out_type, int ca_layers, int tile, int order,
-              int sched, void* ws, size_t ws_bytes, void* stream_ptr, bool f8 = false) {
+              int sched, void* ws, size_t ws_bytes, void* stream_ptr, int f8 = 0) {
   const sfc::Checked chk =
       f8 ? sfc::check_gemm_f8_args(M, N, K, A, lda, B, ldb, C, ldc, out_type, ca_layers, tile, order, sched, ws,
                                    ws_bytes)
@@ -279,11 +279,11 @@ int gemm_impl(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const
     const int64_t slots = (int64_t)st->num_cus * main.occ;
     main.grid = (int)(tasks < slots ? tasks : slots);
     const int64_t n1 = (int64_t)main.gn * main.bn;
-    rc = launch_plan(*st, main, M, n1, K, A, lda, B, ldb, C, ldc, 0, ob, order, sched, stream, false);
+    rc = launch_plan(*st, main, M, n1, K, A, lda, B, ldb, C, ldc, 0, ob, order, sched, stream, 0);
     if (rc != SFC_OK) return rc;
     const size_t esz = ob ? 2 : 4;
     return launch_plan(*st, sp.strip, M, N - n1, K, A, lda, static_cast<const uint16_t*>(B) + n1, ldb,
-                       static_cast<char*>(C) + (size_t)n1 * esz, ldc, 0, ob, order, sched, stream, false);
+                       static_cast<char*>(C) + (size_t)n1 * esz, ldc, 0, ob, order, sched, stream, 0);
   }
 
   float* W = nullptr;
@@ -373,7 +373,16 @@ int sfc_gemm_f8_ex(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, 
                    int64_t ldb, void* C, int64_t ldc, int out_type, int ca_layers, int tile, int order,
                    int sched, void* ws, size_t ws_bytes, void* stream) {
   return gemm_impl(M, N, K, A, lda, B, ldb, C, ldc, out_type, ca_layers, tile, order, sched, ws,
-                   ws_bytes, stream, true);
+                   ws_bytes, stream, 1);
+}
+
+int sfc_gemm_f8_fmt_ex(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* B,
+                       int64_t ldb, void* C, int64_t ldc, int out_type, int a_format, int b_format,
+                       int ca_layers, int tile, int order, int sched, void* ws, size_t ws_bytes, void* stream) {
+  if ((a_format != SFC_FP8_E4M3 && a_format != SFC_FP8_E5M2) || (b_format != SFC_FP8_E4M3 && b_format != SFC_FP8_E5M2))
+    return set_error(SFC_ERR_INVALID_ARG, "unknown fp8 format");
+  return gemm_impl(M, N, K, A, lda, B, ldb, C, ldc, out_type, ca_layers, tile, order, sched, ws,
+                   ws_bytes, stream, 1 + a_format + 2 * b_format);
 }
 
 int sfc_gemm(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* B, int64_t ldb,

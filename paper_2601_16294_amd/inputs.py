@@ -55,12 +55,21 @@ def draw(rows: int, cols: int, dist: Tuple, seed: int, ld: Optional[int] = None)
 
 
 NAN_E4M3 = 0x7F
+NAN_E5M2 = 0x7F
 
 
 def draw_e4m3(rows: int, cols: int, dist: Tuple, seed: int, ld: Optional[int] = None) -> np.ndarray:
     """A rows x ld uint8 array of OCP FP8 E4M3 codes (drawn in fp32 as in draw()
     and converted by torch's float8_e4m3fn cast, round to nearest even);
     columns >= cols hold the NaN code."""
+    return draw_fp8(rows, cols, dist, seed, ld, "e4m3")
+
+
+def draw_fp8(rows: int, cols: int, dist: Tuple, seed: int, ld: Optional[int] = None,
+             fmt: str = "e4m3") -> np.ndarray:
+    """draw_e4m3 for either OCP format: fmt "e4m3" (torch.float8_e4m3fn) or
+    "e5m2" (torch.float8_e5m2); columns >= cols hold that format's NaN code."""
+    dtype = {"e4m3": torch.float8_e4m3fn, "e5m2": torch.float8_e5m2}[fmt]
     ld = cols if ld is None else ld
     if ld < cols:
         raise ValueError("ld < cols")
@@ -74,9 +83,9 @@ def draw_e4m3(rows: int, cols: int, dist: Tuple, seed: int, ld: Optional[int] = 
         x = rng.integers(dist[1], dist[2] + 1, size=(rows, cols)).astype(np.float32)
     else:
         raise ValueError(kind)
-    out = np.full((rows, ld), NAN_E4M3, dtype=np.uint8)
+    out = np.full((rows, ld), NAN_E4M3 if fmt == "e4m3" else NAN_E5M2, dtype=np.uint8)
     if rows and cols:
-        t = torch.from_numpy(np.ascontiguousarray(x)).to(torch.float8_e4m3fn)
+        t = torch.from_numpy(np.ascontiguousarray(x)).to(dtype)
         out[:, :cols] = t.view(torch.uint8).numpy()
     return out
 

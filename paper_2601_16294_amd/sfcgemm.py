@@ -34,7 +34,7 @@ SCHEDS = {"interleaved": 0, "block": 1, "interleaved_plain": 2}
 
 # Every symbol include/sfcgemm.h declares.
 EXPORTS = ["sfc_tile_order", "sfc_tile_order_ex", "sfc_gemm", "sfc_gemm_bf16out", "sfc_gemm_ws_size",
-           "sfc_gemm_ex", "sfc_gemm_f8_ex", "sfc_gemm_plan", "sfc_gemm_model", "sfc_probe_mfma", "sfc_strerror",
+           "sfc_gemm_ex", "sfc_gemm_f8_ex", "sfc_gemm_f8_fmt_ex", "sfc_gemm_plan", "sfc_gemm_model", "sfc_probe_mfma", "sfc_strerror",
            "sfc_last_error", "sfc_version"]
 
 
@@ -62,6 +62,9 @@ def _load() -> ctypes.CDLL:
     lib.sfc_gemm_ex.restype = i32
     lib.sfc_gemm_f8_ex.argtypes = [i64, i64, i64, p, i64, p, i64, p, i64, i32, i32, i32, i32, i32, p, sz, p]
     lib.sfc_gemm_f8_ex.restype = i32
+    lib.sfc_gemm_f8_fmt_ex.argtypes = [i64, i64, i64, p, i64, p, i64, p, i64, i32, i32, i32, i32, i32, i32, i32, p,
+                                       sz, p]
+    lib.sfc_gemm_f8_fmt_ex.restype = i32
     lib.sfc_gemm_ws_size.argtypes = [i64, i64, i64, i32]
     lib.sfc_gemm_ws_size.restype = sz
     lib.sfc_gemm_plan.argtypes = [i64, i64, i64, i32, i32, ctypes.POINTER(ctypes.c_int64)]
@@ -175,11 +178,17 @@ def sfc_gemm_ex(A, B, C, ca_layers: int = 1, tile: str = "auto", order: str = "h
            "sfc_gemm_ex")
 
 
+FP8_FORMATS = {"e4m3": 0, "e5m2": 1}
+
+
 def sfc_gemm_f8_ex(A, B, C, ca_layers: int = 1, tile: str = "auto", order: str = "hilbert",
-                   sched: str = "interleaved", workspace=None, stream=None) -> None:
-    """C = A @ B with OCP FP8 E4M3 operands.  A: (M, K) and B: (K, N) CUDA
-    tensors of E4M3 bytes (torch.uint8 or torch.float8_e4m3fn), C: (M, N)
-    float32 or bfloat16, all with unit column stride."""
+                   sched: str = "interleaved", workspace=None, stream=None, a_format: str = "e4m3",
+                   b_format: str = "e4m3") -> None:
+    """C = A @ B with OCP 8-bit float operands.  A: (M, K) and B: (K, N) CUDA
+    tensors of fp8 bytes (torch.uint8, or torch.float8_e4m3fn / float8_e5m2),
+    each in its format ("e4m3" or "e5m2"); C: (M, N) float32 or bfloat16, all
+    with unit column stride.  Both formats E4M3 call sfc_gemm_f8_ex, any other
+    pair sfc_gemm_f8_fmt_ex."""
     import torch
     pa, M, K, lda = _matrix(A, "A")
     pb, K2, N, ldb = _matrix(B, "B")
@@ -187,8 +196,9 @@ def sfc_gemm_f8_ex(A, B, C, ca_layers: int = 1, tile: str = "auto", order: str =
     if K2 != K or M2 != M or N2 != N:
         raise ValueError(f"shape mismatch: A {tuple(A.shape)} B {tuple(B.shape)} C {tuple(C.shape)}")
     for t, n in ((A, "A"), (B, "B")):
-        if t.dtype not in (torch.uint8, torch.int8, torch.float8_e4m3fn):
-            raise TypeError(f"{n} must hold E4M3 bytes")
+        if t.dtype not in (torch.uint8, torch.int8, torch.float8_e4m3fn, torch.float8_e5m2):
+            raise TypeError(f"{n} must hold fp8 bytes")
+    fa, fb = FP8_FORMATS[a_format], FP8_FORMATS[b_format]
     if C.dtype == torch.float32:
         out = SFC_OUT_F32
     elif C.dtype == torch.bfloat16:
@@ -197,9 +207,14 @@ def sfc_gemm_f8_ex(A, B, C, ca_layers: int = 1, tile: str = "auto", order: str =
         raise TypeError("C must be float32 or bfloat16")
     ws_ptr, ws_bytes = (None, 0) if workspace is None else (workspace.data_ptr(),
                                                             workspace.numel() * workspace.element_size())
-    _check(lib.sfc_gemm_f8_ex(M, N, K, pa, lda, pb, ldb, pc, ldc, out, ca_layers, TILES[tile],
-                              ORDERS[order], SCHEDS[sched], ws_ptr, ws_bytes, _stream_handle(stream)),
-           "sfc_gemm_f8_ex")
+    if fa == 0 and fb == 0:
+        _check(lib.sfc_gemm_f8_ex(M, N, K, pa, lda, pb, ldb, pc, ldc, out, ca_layers, TILES[tile],
+                                  ORDERS[order], SCHEDS[sched], ws_ptr, ws_bytes, _stream_handle(stream)),
+               "sfc_gemm_f8_ex")
+    else:
+        _check(lib.sfc_gemm_f8_fmt_ex(M, N, K, pa, lda, pb, ldb, pc, ldc, out, fa, fb, ca_layers, TILES[tile],
+                                      ORDERS[order], SCHEDS[sched], ws_ptr, ws_bytes, _stream_handle(stream)),
+               "sfc_gemm_f8_fmt_ex")
 
 
 def to_device_u8(bits: np.ndarray, device="cuda"):

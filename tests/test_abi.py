@@ -154,3 +154,13 @@ def test_f8_invalid_arguments_rejected_before_any_launch(sg, kw, code):
 def test_f8_empty_output_is_a_noop(sg):
     assert call_f8(sg, M=0, C=None, A=None) == 0
     assert call_f8(sg, N=0, C=None, B=None) == 0
+
+
+def test_f8_format_codes_validated(sg):
+    args = (64, 64, 64, 4096, 64, 8192, 64, 16384, 64, F32)
+    tail = (1, 0, 0, 0, None, 0, None)
+    for fa, fb in ((2, 0), (0, 2), (-1, 0), (0, 5)):
+        assert sg.lib.sfc_gemm_f8_fmt_ex(*args, fa, fb, *tail) == -1
+        assert "format" in sg.last_error()
+    # valid codes reach the other checks: a misaligned A is still rejected
+    assert sg.lib.sfc_gemm_f8_fmt_ex(64, 64, 64, 4096 + 8, 64, 8192, 64, 16384, 64, F32, 1, 1, *tail) == -2

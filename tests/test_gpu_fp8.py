@@ -10,7 +10,7 @@ from oracle import bf16 as obf16
 from oracle import check as ocheck
 from oracle import fp8 as of8
 from oracle import gemm as ogemm
-from paper_2601_16294_amd.inputs import NAN_E4M3, draw_e4m3
+from paper_2601_16294_amd.inputs import NAN_E4M3, draw_e4m3, draw_fp8
 from gpu_util import raw_bits, sg, to_host
 
 pytestmark = pytest.mark.gpu
@@ -130,3 +130,60 @@ def test_auto_layers(M, N, K):
     pick = sg().sfc_gemm_model(M, N, 64 * -(-K // 128), out="f32", tile="256x256")
     if (M, N, K) == (1024, 1024, 16384):
         assert pick["layers"] > 1
+
+
+# ---- OCP E5M2 and mixed formats (sfc_gemm_f8_fmt_ex) ---------------------------
+
+FMT_PAIRS = [("e5m2", "e5m2"), ("e4m3", "e5m2"), ("e5m2", "e4m3")]
+
+
+def ref_fmt(A8, B8, M, N, K, fa, fb):
+    A = of8.to_bf16_bits(A8[:, :K], fa)
+    B = of8.to_bf16_bits(B8[:, :N], fb)
+    return ogemm.gemm_ref_rows(A, B, N, K, K, N, M=M)
+
+
+@pytest.mark.parametrize("fa,fb", FMT_PAIRS)
+@pytest.mark.parametrize("M,N,K,c,out", [(300, 528, 400, 1, "f32"), (513, 272, 1040, 3, "bf16"),
+                                         (256, 256, 256, 2, "f32"), (7, 32, 48, 1, "bf16")])
+def test_formats_against_oracle(fa, fb, M, N, K, c, out):
+    seed = 9700 + M + 3 * K + (fa == "e5m2") + 2 * (fb == "e5m2")
+    A = draw_fp8(M, K, ("normal", 0.0, 1.0), seed, fmt=fa)
+    B = draw_fp8(K, N, ("normal", 0.0, 1.0), seed + 1, fmt=fb)
+    Cr, R = ref_fmt(A, B, M, N, K, fa, fb)
+    dtype = torch.float32 if out == "f32" else torch.bfloat16
+    C = torch.full((M, N), float("nan"), dtype=dtype, device="cuda")
+    sg().sfc_gemm_f8_ex(up8(A), up8(B), C, ca_layers=c, a_format=fa, b_format=fb)
+    torch.cuda.synchronize()
+    ocheck.assert_gemm_close(to_host(C), Cr, R, f"{fa} x {fb} {M}x{N}x{K} c={c} {out}")
+
+
+@pytest.mark.parametrize("fa,fb", FMT_PAIRS)
+def test_formats_integers_exact(fa, fb):
+    """Integers in [-8, 8] are exact in both formats; sums stay below 2^24."""
+    M, N, K = 260, 304, 1024
+    A = draw_fp8(M, K, ("int", -8, 8), 9801, fmt=fa)
+    B = draw_fp8(K, N, ("int", -8, 8), 9802, fmt=fb)
+    Cr, _ = ref_fmt(A, B, M, N, K, fa, fb)
+    for c in (1, 4):
+        C = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
+        sg().sfc_gemm_f8_ex(up8(A), up8(B), C, ca_layers=c, a_format=fa, b_format=fb)
+        torch.cuda.synchronize()
+        assert np.array_equal(to_host(C), Cr), f"{fa} x {fb} c={c}"
+
+
+def test_format_codes_select_the_format():
+    """The same bytes read as E4M3 and as E5M2 give the two oracles' results
+    (a swapped or ignored format code fails one of them)."""
+    M, N, K = 256, 256, 512
+    A = draw_fp8(M, K, ("normal", 0.0, 0.5), 9901, fmt="e4m3")
+    B = draw_fp8(K, N, ("normal", 0.0, 0.5), 9902, fmt="e4m3")
+    # reinterpret B's bytes in the other format too (codes 0x7C-0x7F and
+    # 0xFC-0xFF are infinities or NaN in E5M2: clear them to keep values finite)
+    B5 = np.where((B & 0x7C) == 0x7C, B & 0x83, B).astype(np.uint8)
+    for fb, Bx in (("e4m3", B5), ("e5m2", B5)):
+        Cr, R = ref_fmt(A, Bx, M, N, K, "e4m3", fb)
+        C = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
+        sg().sfc_gemm_f8_ex(up8(A), up8(Bx), C, a_format="e4m3", b_format=fb)
+        torch.cuda.synchronize()
+        ocheck.assert_gemm_close(to_host(C), Cr, R, f"bytes read as {fb}")
