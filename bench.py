@@ -9,14 +9,18 @@ output), timed over K back-to-back calls with inputs resident in HBM.  The
 line also carries:
   * roofline   -- the GEMM kernel's own average duration (HIP events on the
                   launch stream over the timed steps) against the bf16 dense
-                  MFMA peak;
+                  MFMA peak, HBM bytes per launch from committed counter runs,
+                  the sustained MFMA probe, and the same kernel on constant
+                  operands (full clock: the kernel's per-clock efficiency);
   * cpu_baseline -- the CPU oracle on a bounded row sample of the same GEMM;
   * workloads  -- every measured workload (TFLOP/s, cold and warm, the paper's
                   protocol of 10 cold repetitions) and their flop-weighted
-                  harmonic mean;
+                  harmonic mean; for the K-dominant one also the layers placed
+                  on whole chiplets against the hardware workgroup order;
   * fp8_square8192 -- the same 8192^3 GEMM with OCP FP8 E4M3 operands
                   (sfc_gemm_f8_ex, bf16 output), timed like the headline,
-                  against the fp8 dense MFMA peak;
+                  against the fp8 dense MFMA peak, with the vendor library's
+                  fp8 GEMM beside it and an E5M2 line (sfc_gemm_f8_fmt_ex);
   * sweep      -- with --sweep: the paper's 125-shape cube sweep (Section IV.A),
                   per shape the library's own choice of block shape and layer
                   count (10 cold repetitions), the best of a small autotune

@@ -218,7 +218,7 @@ def sfc_gemm_f8_ex(A, B, C, ca_layers: int = 1, tile: str = "auto", order: str =
 
 
 def to_device_u8(bits: np.ndarray, device="cuda"):
-    """Upload a uint8 array (E4M3 patterns) as a torch.uint8 CUDA tensor."""
+    """Upload a uint8 array (fp8 patterns) as a torch.uint8 CUDA tensor."""
     import torch
     return torch.from_numpy(np.ascontiguousarray(bits, dtype=np.uint8)).to(device)
 
