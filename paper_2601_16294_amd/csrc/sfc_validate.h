@@ -96,6 +96,21 @@ inline size_t ws_size(int64_t M, int64_t N, int64_t K, int ca_layers) {
   return (size_t)ce * (size_t)M * (size_t)N * 4u;
 }
 
+// Block columns that a half-height strip takes over (0: none).  A grid of
+// gm x gn blocks on `slots` resident workgroups leaves r = gm*gn mod slots
+// blocks in its last round; when 0 < r <= slots/2 the last w = ceil(r/gm)
+// block columns go to blocks of half the height, `half_rows` rows of them,
+// provided those fit in one round of `half_slots` workgroups and w < gn.
+inline int strip_columns(int gm, int gn, int64_t slots, int64_t half_rows, int64_t half_slots) {
+  if (gm <= 0 || gn <= 0 || slots <= 0) return 0;
+  const int64_t T = (int64_t)gm * gn;
+  const int64_t r = T % slots;
+  if (T <= slots || r == 0 || 2 * r > slots) return 0;
+  const int64_t w = ceil_div(r, gm);
+  if (w >= gn || half_rows * w > half_slots) return 0;
+  return (int)w;
+}
+
 // 16-byte loads are legal when every row starts 16-byte aligned and the K and
 // N extents end on whole 8-element chunks.
 inline bool vector_loads_ok(const void* A, int64_t lda, const void* B, int64_t ldb, int64_t K,

@@ -191,29 +191,26 @@ int plan_tail_split(DeviceState& st, const Plan& pl, int64_t M, int64_t N, int64
   if (pl.tile == sfc::kT256x256) half = sfc::kT128x256;
   else if (pl.tile == sfc::kT256x128) half = sfc::kT128x128;
   else return SFC_OK;
-  const int64_t T = (int64_t)pl.gm * pl.gn;
-  const int64_t S = (int64_t)st.num_cus * pl.occ;
-  const int64_t r = T % S;
-  if (T <= S || r == 0 || 2 * r > S) return SFC_OK;
-  const int w = (int)sfc::ceil_div(r, pl.gm);
-  if (w >= pl.gn) return SFC_OK;
   int occ2 = 1;
   int rc = get_occupancy(st, half, ob, true, &occ2);
   if (rc != SFC_OK) return rc;
+  const int64_t half_rows = sfc::ceil_div(M, sfc::tile_bm(half));
+  const int w = sfc::strip_columns(pl.gm, pl.gn, (int64_t)st.num_cus * pl.occ, half_rows,
+                                   (int64_t)st.num_cus * occ2);
+  if (w == 0) return SFC_OK;
   Plan& q = sp->strip;
   q.tile = half;
   q.bm = sfc::tile_bm(half);
   q.bn = sfc::tile_bn(half);
   const int64_t n1 = (int64_t)(pl.gn - w) * pl.bn;
-  q.gm = (int)sfc::ceil_div(M, q.bm);
+  q.gm = (int)half_rows;
   q.gn = (int)sfc::ceil_div(N - n1, q.bn);
   q.ce = 1;
   q.nk = pl.nk;
   q.occ = occ2;
   q.vec = sfc::vector_loads_ok(A, lda, static_cast<const uint16_t*>(B) + n1, ldb, K, N - n1);
-  const int64_t tasks = (int64_t)q.gm * q.gn;
-  if (!q.vec || tasks > (int64_t)st.num_cus * occ2) return SFC_OK;
-  q.grid = (int)tasks;
+  if (!q.vec) return SFC_OK;
+  q.grid = (int)((int64_t)q.gm * q.gn);
   sp->w = w;
   sp->on = true;
   return SFC_OK;
