@@ -409,9 +409,17 @@ def main():
                 log(f"[bench] {name} placement: {entry['layer_placement']}")
             best_c = max(per_c, key=lambda k: per_c[k]["tflops_cold"])
             best = per_c[best_c]
+            # roofline of the workload: min(MFMA peak, OI x HBM) per GEMM with its
+            # compulsory bytes (A, B and C once), times summed over the GEMMs
+            roofs = [roofline_tflops(x.M, x.N, x.K, 2 if x.out == "bf16" else 4) for x in wl.gemms]
+            t_roof = sum(2.0 * x.M * x.N * x.K / (r[1] * 1e12) for x, r in zip(wl.gemms, roofs))
+            roof = wl.flops / t_roof / 1e12
             entry.update({"per_ca_layers": per_c if len(per_c) > 1 else None, "best_ca_layers": best_c,
                           "tflops": best["tflops_cold"], "tflops_warm": best["tflops_warm"],
-                          "frac_of_mfma_peak": round(best["tflops_cold"] / PEAK_BF16_TFLOPS, 4)})
+                          "frac_of_mfma_peak": round(best["tflops_cold"] / PEAK_BF16_TFLOPS, 4),
+                          "roofline_bound": "hbm" if any(r[0] == "hbm" for r in roofs) else "mfma",
+                          "roofline_tflops": round(roof, 1),
+                          "frac_of_roofline": round(best["tflops_cold"] / roof, 4)})
             table[name] = entry
             whm_num += wl.flops
             whm_den += wl.flops / best["tflops_cold"]
