@@ -106,11 +106,16 @@ int sfc_tile_order_ex(int gm, int gn, int order, int32_t *out_idx);
  *              (64 deep) are split into min(c, ceil(K/64)) contiguous ranges,
  *              range l holding blocks [floor(l*nK/c), floor((l+1)*nK/c)).  For
  *              c > 1 the partial copies live in a workspace of
- *              sfc_gemm_ws_size() bytes that the library allocates once per
- *              device and reuses; concurrent c > 1 calls on different streams
- *              must use sfc_gemm_ex with their own workspaces.
+ *              sfc_gemm_ws_size() bytes that the library keeps per stream: it
+ *              is allocated, and grown, in stream order (hipMallocAsync /
+ *              hipFreeAsync on `stream`), and only work on that stream uses
+ *              it, so calls on different streams may run concurrently.  It is
+ *              kept, keyed by the stream handle, until the process ends.
  *              SFC_CA_AUTO (0): the model picks c (see sfc_gemm_model).
  *   stream     hipStream_t or NULL.
+ * No GEMM entry point synchronises the device or a stream.  The first call for
+ * a block grid allocates its curve table (hipMalloc) and enqueues the
+ * generator on `stream`; calls on other streams wait for it on the device.
  */
 int sfc_gemm(int64_t M, int64_t N, int64_t K,
              const void *A, int64_t lda,
@@ -126,8 +131,10 @@ int sfc_gemm_bf16out(int64_t M, int64_t N, int64_t K,
                      int ca_layers, void *stream);
 
 /*
- * sfc_gemm_ws_size -- bytes of fp32 workspace that a ca_layers = c call needs:
- * c_eff * M * N * 4 with c_eff = min(c, ceil(K/64)) when c_eff > 1, else 0.
+ * sfc_gemm_ws_size -- bytes of fp32 workspace that a ca_layers = c call needs
+ * for the replicated C of Section II.C / II.D (Listing 1 keeps K_layers copies
+ * of C, one per K range, and reduces them): c_eff dense M x N fp32 copies,
+ * c_eff * M * N * 4 bytes with c_eff = min(c, ceil(K/64)) when c_eff > 1, else 0.
  * For c = SFC_CA_AUTO: the size for the largest count the model picks (16), a
  * bound that holds whatever it chooses.  Returns 0 for invalid arguments as well.
  */
@@ -149,6 +156,28 @@ int sfc_gemm_ex(int64_t M, int64_t N, int64_t K,
                 void *C, int64_t ldc,
                 int out_type, int ca_layers, int tile, int order, int sched,
                 void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * sfc_gemm_fused_ex -- sfc_gemm_ex with the reduction of the layer copies
+ * fused into the GEMM launch (Listing 1's final add-reduce, Section II.D,
+ * done by the GEMM's own workgroups): the workgroup that finishes a block's
+ * layer copy publishes it (a release fence at device scope) and counts it on
+ * the block's arrival counter (a device-scope atomic); the workgroup that
+ * completes the count reads the c_eff copies of that block and sums them in
+ * ascending layer order in fp32, so C is bit-identical to sfc_gemm_ex's.  No
+ * workgroup waits for another.  One launch instead of two; the c_eff-way sum of
+ * a block runs on one compute unit.  The counters are library memory kept per
+ * stream (zero between launches; a call never leaves one raised), so `ws`, if
+ * given, still needs only sfc_gemm_ws_size() bytes.  With c_eff = 1 this is
+ * sfc_gemm_ex.  Arguments, errors and the contents left in ws as for
+ * sfc_gemm_ex.
+ */
+int sfc_gemm_fused_ex(int64_t M, int64_t N, int64_t K,
+                      const void *A, int64_t lda,
+                      const void *B, int64_t ldb,
+                      void *C, int64_t ldc,
+                      int out_type, int ca_layers, int tile, int order, int sched,
+                      void *ws, size_t ws_bytes, void *stream);
 
 /*
  * sfc_gemm_f8_ex -- C = A * B with 8-bit float operands (the paper leaves the

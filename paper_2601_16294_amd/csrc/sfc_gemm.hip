@@ -11,9 +11,8 @@
 // fp32 workspace layer that a separate reduction sums.
 //
 // Mapping to the chip:
-//   * one workgroup = 4 waves (2 x 2; one per SIMD), each wave owns a
-//     (BM/2) x (BN/2) sub-block held as 16x16 fp32 MFMA accumulators; the
-//     fast path can also run 8 waves (2 x 4, two per SIMD) per workgroup;
+//   * one workgroup = 4 waves (one per SIMD; 2 x 2, or 1 x 4 for 128x256
+//     blocks), each wave owning its sub-block as 16x16 fp32 MFMA accumulators;
 //   * the grid is persistent: P workgroups, P = CUs x occupancy, each looping
 //     over tasks.  Hardware deals workgroup b to chiplet (XCD) b % 8; ranks are
 //     renumbered so that each XCD's workgroups hold consecutive ranks, and with
@@ -150,19 +149,15 @@ __device__ __forceinline__ void wait_lds_all() { asm volatile("s_waitcnt lgkmcnt
 // The MFMA takes the B fragment as its first operand, so it computes the
 // transposed 16x16 block: lane l ends with row l%16 of the fragment and its 4
 // consecutive columns 4*(l/16) .. +3.
-// NW waves per workgroup in a WGM x WGN grid: 4 waves (one per SIMD) or 8
-// (two per SIMD, so that one wave's MFMAs run while the other issues its reads,
-// loads and waits).  A wave's fragment reads per 32-deep step are FM b128
-// reads of A and 2*FN transposing reads of B, so the grid keeps the wave
-// sub-block at most twice as wide as tall.
+// NW = 4 waves per workgroup (one per SIMD) in a WGM x WGN grid.  A wave's
+// fragment reads per 32-deep step are FM b128 reads of A and 2*FN transposing
+// reads of B, so the grid keeps the wave sub-block at most twice as wide as
+// tall: 2 x 2 waves, except 1 x 4 for 128x256 blocks (128x64 per wave).
 template <int BM, int BN, int NW, int F8>
 struct Tile {
-  static_assert(NW == 4 || NW == 8, "4 or 8 waves");
+  static_assert(NW == 4, "4 waves");
   static constexpr int THREADS = NW * 64;
-#ifndef SFC_WGM_128x256
-#define SFC_WGM_128x256 1
-#endif
-  static constexpr int WGM = (NW == 4 && BM == 128 && BN == 256) ? SFC_WGM_128x256 : 2;  // waves along M
+  static constexpr int WGM = (BM == 128 && BN == 256) ? 1 : 2;  // waves along M
   static constexpr int WGN = NW / WGM;                // waves along N
   static constexpr int WTM = BM / WGM, WTN = BN / WGN;  // wave sub-block
   // fragments per wave: 16x16 (bf16, MFMA 16x16x32) or 32x32 (fp8, MFMA 32x32x64)
@@ -255,7 +250,7 @@ __device__ __forceinline__ void mma_step(const Frags<BM, BN, NW, F8>& cur, Acc<B
 // Every instruction of the loop counts: with one wave per SIMD a wave issues
 // at most one instruction per four clocks, so the loop keeps its other work
 // (LDS reads, loads, address arithmetic) to a few instructions per MFMA,
-// spread evenly.  (With 8 waves two waves share a SIMD and interleave.)
+// spread evenly.
 constexpr int kSK = 32;        // K depth of one B stage (one MFMA step)
 constexpr int kBias = 4096;    // bytes; keeps every biased voffset positive
 
@@ -707,14 +702,15 @@ __device__ __forceinline__ void ring_step(Acc<BM, BN, NW, F8>& acc, const Frags<
 struct RingAddr {
   uint64_t a0, b0;           // byte address of the first block's A origin and B origin, minus kBias
   uint64_t b_step;           // bytes between consecutive B stages (32 rows of B)
-  int x_part;                // first B stage that is not wholly before row K
-  uint32_t lim_part;         // its num_records: its rows before K, plus the bias
+  int x_part;                // first B stage that is not wholly before the task's K end
+  uint32_t lim_part;         // its num_records: its rows before that end, plus the bias
   uint32_t lds0;             // LDS byte address of the ring
   int wave;
 };
 
-// num_records of B stage x: rows at or past K fall outside and read zeros (a
-// stage wholly past K reads nothing from memory)
+// num_records of B stage x: rows at or past the task's K end (row K, or the
+// end of its layer's K range) fall outside and read zeros (a stage wholly past
+// that end reads nothing from memory)
 __device__ __forceinline__ uint32_t b_stage_limit(const RingAddr& ra, int x) {
   return x < ra.x_part ? (uint32_t)kOobOffset : x == ra.x_part ? ra.lim_part : (uint32_t)kBias;
 }
@@ -1045,6 +1041,41 @@ __device__ __forceinline__ void store_tile32(const GemmParams& p, const Acc<BM, 
   }
 }
 
+// ---- stores of layer copies that the fused reduction reads ------------------------------------
+// With `co` set, a store is made at device scope: written through this
+// chiplet's L2 to the device's coherence point, so that once the wave's stores
+// have completed (vmcnt 0) a workgroup on another chiplet can read them with
+// device-scope loads, without an L2 write-back or invalidation.  `co` is
+// wave-uniform; the choice is a scalar branch inside the store itself, so that
+// the compiler keeps one copy of the epilogue (two copies raise the register
+// pressure of the kernel past its budget).  The compiler treats the data
+// registers as free once the statement ends, but a 16-byte store still reads
+// them after it issues: the trailing s_nop keeps the next vector instruction
+// from overwriting them too early (the compiler inserts the same wait states
+// after its own stores).
+__device__ __forceinline__ void st16_co(void* p, u32x4 v, int co) {
+  asm volatile("s_cmp_eq_u32 %2, 0\n\t"
+               "s_cbranch_scc1 1f\n\t"
+               "global_store_dwordx4 %0, %1, off sc1\n\t"
+               "s_branch 2f\n"
+               "1:\n\t"
+               "global_store_dwordx4 %0, %1, off\n"
+               "2:\n\t"
+               "s_nop 1"
+               :: "v"(p), "v"(v), "s"(__builtin_amdgcn_readfirstlane(co)) : "memory", "scc");
+}
+// 16 bytes of an epilogue store: device scope when the kernel may fuse the
+// reduction (fp32 layer copies) and `co` is set, else a plain store.
+template <bool FUSABLE>
+__device__ __forceinline__ void st16(void* p, u32x4 v, int co) {
+  if constexpr (FUSABLE) st16_co(p, v, co);
+  else *reinterpret_cast<u32x4*>(p) = v;
+}
+__device__ __forceinline__ void st_f32(float* p, float v, int co) {
+  if (co) __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  else *p = v;
+}
+
 // ---- epilogue through LDS (fast path) ------------------------------------------------------
 // After a task's K loop the rings are free.  Each wave writes its sub-block to
 // its own LDS region, rows padded by 16 bytes (the fragment writes, 16 rows at
@@ -1088,7 +1119,7 @@ __device__ __forceinline__ u32x4 lds_read16(uint32_t addr) {
 template <int BM, int BN, int NW, int F8, bool OUT_BF16>
 __device__ __forceinline__ void store_tile_staged(const GemmParams& p, const Acc<BM, BN, NW, F8>& acc, int64_t m0,
                                                   int64_t n0, int64_t lstride, int wm, int wn, int wave, int lane,
-                                                  uint32_t lds0) {
+                                                  uint32_t lds0, int co) {
   using T = Tile<BM, BN, NW, F8>;
   using S = Staging<BM, BN, NW, F8, OUT_BF16>;
   typedef typename std::conditional<OUT_BF16, __bf16, float>::type OutT;
@@ -1160,7 +1191,7 @@ __device__ __forceinline__ void store_tile_staged(const GemmParams& p, const Acc
       for (int u = 0; u < 4; ++u)
         if (t + u < S::PASS_ROWS / S::RPI) {
           const int64_t row = row0 + pass * S::PASS_ROWS + (t + u) * S::RPI + rr;
-          *reinterpret_cast<u32x4*>(out + row * p.ldo + col0 + cc * (16 / S::ES)) = v[u];
+          st16<!OUT_BF16 && F8 == 0>(out + row * p.ldo + col0 + cc * (16 / S::ES), v[u], co);
         }
     }
     if (pass + 1 < S::PASSES) wait_lds_all();   // this wave's reads are done before its next writes
@@ -1169,7 +1200,7 @@ __device__ __forceinline__ void store_tile_staged(const GemmParams& p, const Acc
 
 template <int BM, int BN, int NW, int F8, bool OUT_BF16>
 __device__ __forceinline__ void store_tile(const GemmParams& p, const Acc<BM, BN, NW, F8>& acc, int64_t m0, int64_t n0,
-                                           int64_t lstride, int wm, int wn, int lane, bool fast, bool fast16) {
+                                           int64_t lstride, int wm, int wn, int lane, bool fast, bool fast16, int co) {
   if constexpr (F8 != 0) {
     store_tile32<BM, BN, NW, OUT_BF16>(p, acc, m0, n0, lstride, wm, wn, lane, fast, fast16);
     return;
@@ -1209,7 +1240,17 @@ __device__ __forceinline__ void store_tile(const GemmParams& p, const Acc<BM, BN
           bf16x4 v = {(__bf16)acc[i][j][0], (__bf16)acc[i][j][1], (__bf16)acc[i][j][2], (__bf16)acc[i][j][3]};
           *reinterpret_cast<bf16x4*>(row + j * 16) = v;
         } else {
-          *reinterpret_cast<f32x4*>(row + j * 16) = acc[i][j];
+          if (F8 == 0 && co) {
+            // device scope, as two 8-byte atomic stores (an inline-assembly
+            // store would copy the accumulators out of their registers first)
+            typedef uint64_t u64x2 __attribute__((ext_vector_type(2)));
+            const u64x2 w = __builtin_bit_cast(u64x2, acc[i][j]);
+            uint64_t* q = reinterpret_cast<uint64_t*>(row + j * 16);
+            __hip_atomic_store(q, w[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(q + 1, w[1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          } else {
+            *reinterpret_cast<f32x4*>(row + j * 16) = acc[i][j];
+          }
         }
       }
       // keep the scheduler from converting every accumulator before storing any
@@ -1227,11 +1268,109 @@ __device__ __forceinline__ void store_tile(const GemmParams& p, const Acc<BM, BN
       const int64_t c = c0 + j * 16;
 #pragma unroll
       for (int e = 0; e < 4; ++e)
-        if (c + e < p.N) row[c + e] = (OutT)acc[i][j][e];
+        if (c + e < p.N) {
+          if constexpr (OUT_BF16) row[c + e] = (OutT)acc[i][j][e];
+          else st_f32(reinterpret_cast<float*>(row) + c + e, acc[i][j][e], co);
+        }
     }
     if (OUT_BF16) __builtin_amdgcn_sched_barrier(0);
   }
   }
+}
+
+// ---- fused reduction of the layer copies ------------------------------------------------
+// Listing 1's final add-reduce over the K layers, done inside the GEMM launch
+// instead of by a separate kernel.  A workgroup stores its layer copy of a
+// block with device-scope stores (written through its chiplet's L2), waits
+// until they have completed, and counts the copy on the block's arrival
+// counter with a device-scope vector atomic: no L2 write-back is needed on
+// this side.  The workgroup whose count completes the block (the last of its
+// c_eff layers to finish) invalidates its chiplet's L2 (an acquire fence at
+// device scope: lines that other chiplets have since overwritten are not read
+// stale), reads every copy and sums them in ascending layer order in fp32,
+// exactly as the separate reduction does (same bits), stores C, and resets
+// the counter to zero for the next launch.  No workgroup ever waits for
+// another.  `flag` is an LDS word that is free at this point (the ring is idle
+// between tasks).
+template <int BM, int BN, int NW>
+__device__ __forceinline__ void fused_finish(const GemmParams& p, int cell, int64_t m0, int64_t n0, int tid,
+                                             int* flag) {
+  constexpr int THREADS = NW * 64;
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this wave's copy has reached the coherence point
+  __syncthreads();
+  if (tid == 0) *flag = __hip_atomic_fetch_add(p.counters + cell, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __syncthreads();
+  const int arrived = *flag;
+  __syncthreads();   // every wave has read the flag before the next task's loads reuse the LDS
+  if (arrived != p.layers - 1) return;
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+
+  const float* W = reinterpret_cast<const float*>(p.out);   // layer copies: dense M x N, ld = N
+  const int64_t ls = p.out_layer_stride;
+  const int layers = p.layers;
+  const int rows = (int)(p.M - m0 < BM ? p.M - m0 : BM);
+  const int cols = (int)(p.N - n0 < BN ? p.N - n0 : BN);
+  const int esz = p.c_bf16 ? 2 : 4;
+  const bool vec = (p.N % 4) == 0 && (p.ldc % 4) == 0 && ((uintptr_t)p.C % (4 * esz)) == 0;
+  if (vec) {
+    // 4 consecutive columns per thread, BN/4 threads per row, U rows per
+    // thread in flight; rows past the block's last re-read that row (in
+    // bounds) and are not stored, so the loads carry no branches
+    constexpr int TPR = BN / 4, RPP = THREADS / TPR, U = 8;
+    const int cg = tid % TPR, r0 = tid / TPR;
+    if (4 * cg < cols) {
+      const int64_t col = n0 + 4 * cg;
+      for (int rb = 0; rb < rows; rb += RPP * U) {
+        const float* src[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int r = rb + u * RPP + r0;
+          src[u] = W + (m0 + (r < rows ? r : rows - 1)) * p.N + col;
+        }
+        f32x4 acc[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) acc[u] = *reinterpret_cast<const f32x4*>(src[u]);
+        for (int l = 1; l < layers; ++l) {
+          f32x4 v[U];
+#pragma unroll
+          for (int u = 0; u < U; ++u) v[u] = *reinterpret_cast<const f32x4*>(src[u] + l * ls);
+#pragma unroll
+          for (int u = 0; u < U; ++u) {
+            acc[u][0] += v[u][0];
+            acc[u][1] += v[u][1];
+            acc[u][2] += v[u][2];
+            acc[u][3] += v[u][3];
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int r = rb + u * RPP + r0;
+          if (r < rows) {
+            const int64_t row = m0 + r;
+            if (p.c_bf16) {
+              const bf16x4 b = {(__bf16)acc[u][0], (__bf16)acc[u][1], (__bf16)acc[u][2], (__bf16)acc[u][3]};
+              *reinterpret_cast<bf16x4*>(reinterpret_cast<__bf16*>(p.C) + row * p.ldc + col) = b;
+            } else {
+              *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(p.C) + row * p.ldc + col) = acc[u];
+            }
+          }
+        }
+      }
+    }
+  } else {
+    // one element per thread, BN (or all) threads per row
+    constexpr int TPR = BN < THREADS ? BN : THREADS, RPP = THREADS / TPR;
+    const int cc0 = tid % TPR, r0 = tid / TPR;
+    for (int rr = r0; rr < rows; rr += RPP)
+      for (int cc = cc0; cc < cols; cc += TPR) {
+        const int64_t idx = (m0 + rr) * p.N + n0 + cc;
+        float sum = W[idx];
+        for (int l = 1; l < layers; ++l) sum += W[l * ls + idx];
+        if (p.c_bf16) reinterpret_cast<__bf16*>(p.C)[(m0 + rr) * p.ldc + n0 + cc] = (__bf16)sum;
+        else reinterpret_cast<float*>(p.C)[(m0 + rr) * p.ldc + n0 + cc] = sum;
+      }
+  }
+  if (tid == 0) __hip_atomic_store(p.counters + cell, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 template <int BM, int BN, int NW, int F8, bool OUT_BF16, bool VEC>
@@ -1310,7 +1449,11 @@ __global__ __launch_bounds__(NW * 64, 1) void sfc_gemm_kernel(GemmParams p) {
         ra.b0 = reinterpret_cast<uint64_t>(Bb + (k0 * p.ldb + n0) * ESZ) - kBias;
         ra.b_step = (uint64_t)SK * (uint64_t)p.ldb * ESZ;
         {
-          const int b_rows = (int)(p.K - k0);   // rows of B from the task's first stage to row K
+          // rows of B from the task's first stage to the end of its layer's K
+          // range (row K for the last layer): the stages that the ring loads
+          // ahead past that point get empty ranges and fetch nothing
+          const int64_t k_end = (int64_t)kt1 * block_k<F8>() < p.K ? (int64_t)kt1 * block_k<F8>() : p.K;
+          const int b_rows = (int)(k_end - k0);
           ra.x_part = b_rows / SK;
           ra.lim_part = (uint32_t)((b_rows % SK) * (int)(p.ldb * ESZ) + kBias);
         }
@@ -1325,9 +1468,13 @@ __global__ __launch_bounds__(NW * 64, 1) void sfc_gemm_kernel(GemmParams p) {
 
     const int64_t lstride = p.out_layer_stride * layer;
     const bool interior = m0 + BM <= p.M && n0 + BN <= p.N;
+    // layer copies that this launch reduces itself are stored coherently
+    constexpr bool kFusable = !OUT_BF16 && F8 == 0;
+    const bool fused = kFusable && p.counters != nullptr;
     if (VEC && Staging<BM, BN, NW, F8, OUT_BF16>::USE && interior && (OUT_BF16 ? vec16_store : vec_store)) {
       if constexpr (VEC && Staging<BM, BN, NW, F8, OUT_BF16>::USE) {
-        store_tile_staged<BM, BN, NW, F8, OUT_BF16>(p, acc, m0, n0, lstride, wm, wn, wave, lane_t, lds_addr(smem));
+        store_tile_staged<BM, BN, NW, F8, OUT_BF16>(p, acc, m0, n0, lstride, wm, wn, wave, lane_t, lds_addr(smem),
+                                                    fused ? 1 : 0);
         // every wave has read its staging rows before the next task's loads
         // land in the rings
         wait_lds_all();
@@ -1335,22 +1482,19 @@ __global__ __launch_bounds__(NW * 64, 1) void sfc_gemm_kernel(GemmParams p) {
       }
     } else {
       store_tile<BM, BN, NW, F8, OUT_BF16>(p, acc, m0, n0, lstride, wm, wn, lane_t, interior && vec_store,
-                                        interior && vec16_store);
+                                        interior && vec16_store, fused ? 1 : 0);
+    }
+    if constexpr (kFusable) {
+      if (fused) fused_finish<BM, BN, NW>(p, cell, m0, n0, tid, reinterpret_cast<int*>(smem));
     }
   }
 }
 
 // ---- dispatch ---------------------------------------------------------------------
-// Waves per workgroup of the fast path for each block shape (the general path
-// always runs 4).  256x256 blocks can be built with 8 waves (two per SIMD,
-// 128x64 each): they need ~3.5 % fewer cycles per launch on MI355X, but read
-// 1.5x the LDS bytes and run at a lower clock for the same time, so 4 is the
-// default.
-#ifndef SFC_WAVES_256x256
-#define SFC_WAVES_256x256 4
-#endif
-static_assert(SFC_WAVES_256x256 == 4 || SFC_WAVES_256x256 == 8, "4 or 8 waves");
-static constexpr int fast_waves(int tile) { return tile == kT256x256 ? SFC_WAVES_256x256 : 4; }
+// Every variant runs 4 waves per workgroup.  (256x256 blocks with 8 waves, two
+// per SIMD and 128x64 each, needed ~3.5 % fewer cycles per launch on MI355X
+// but read 1.5x the LDS bytes and ran at a lower clock for the same time.)
+constexpr int kWaves = 4;
 
 template <int BM, int BN, int NW, int F8, bool OB, bool VEC>
 static const void* kernel_ptr() {
@@ -1377,16 +1521,16 @@ static const void* select_kernel(int tile, bool ob, bool vec) {
   return ob ? (vec ? kernel_ptr<BM_, BN_, NW_, 0, true, true>() : kernel_ptr<BM_, BN_, 4, 0, true, false>()) \
             : (vec ? kernel_ptr<BM_, BN_, NW_, 0, false, true>() : kernel_ptr<BM_, BN_, 4, 0, false, false>())
   switch (tile) {
-    case kT128x128: SFC_K(128, 128, 4);
-    case kT256x128: SFC_K(256, 128, 4);
-    case kT128x256: SFC_K(128, 256, 4);
-    case kT256x256: SFC_K(256, 256, fast_waves(kT256x256));
+    case kT128x128: SFC_K(128, 128, kWaves);
+    case kT256x128: SFC_K(256, 128, kWaves);
+    case kT128x256: SFC_K(128, 256, kWaves);
+    case kT256x256: SFC_K(256, 256, kWaves);
     default: return nullptr;
   }
 #undef SFC_K
 }
 
-static int threads_of(int tile, bool vec) { return (vec ? fast_waves(tile) : 4) * 64; }
+static int threads_of(int, bool) { return kWaves * 64; }
 
 hipError_t launch_gemm(int tile, bool out_bf16, bool vec, const GemmParams& p, int grid,
                        hipStream_t stream, int f8) {

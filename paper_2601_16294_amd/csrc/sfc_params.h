@@ -27,7 +27,12 @@ struct GemmParams {
   int nk;                    // ceil(K / kBK)
   int64_t tasks;             // gm * gn * layers
   int sched;                 // SFC_SCHED_*
-  int pad_;
+  // Fused reduction (layers > 1 and counters != nullptr): the workgroup that
+  // finishes a block's last layer copy sums the copies into C itself.
+  int c_bf16;                // C holds bf16 (else fp32)
+  int32_t* counters;         // per block (im*gn + in): layer copies finished; zero between launches
+  void* C;                   // the final output
+  int64_t ldc;
 };
 
 // Curve table of a gm x gn grid into dev_out (gm*gn int32), order = SFC_ORDER_*.
@@ -41,6 +46,9 @@ hipError_t launch_gemm(int tile, bool out_bf16, bool vec, const GemmParams& p, i
                        hipStream_t stream, int f8 = 0);
 // Workgroups of the given kernel variant that fit on one CU.
 hipError_t gemm_occupancy(int tile, bool out_bf16, bool vec, int* blocks_per_cu, int f8 = 0);
+
+// p[0 .. n) = v (a fill kernel: usable where a memset node is not wanted).
+hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t stream);
 
 // C[i][j] = sum_l W[l][i][j] (ascending l, fp32), W dense M x N per layer.
 hipError_t launch_reduce(const float* W, int layers, int64_t M, int64_t N, void* C, int64_t ldc,

@@ -48,6 +48,19 @@ __global__ __launch_bounds__(256) void sfc_reduce_kernel(const float* __restrict
   }
 }
 
+__global__ __launch_bounds__(256) void sfc_fill_i32_kernel(int32_t* p, int64_t n, int32_t v) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = v;
+}
+
+hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t stream) {
+  if (n <= 0) return hipSuccess;
+  int64_t blocks = (n + 255) / 256;
+  if (blocks > 1024) blocks = 1024;
+  hipLaunchKernelGGL(sfc_fill_i32_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, p, n, v);
+  return hipGetLastError();
+}
+
 hipError_t launch_reduce(const float* W, int layers, int64_t M, int64_t N, void* C, int64_t ldc,
                          bool out_bf16, hipStream_t stream) {
   const int64_t total = M * N;

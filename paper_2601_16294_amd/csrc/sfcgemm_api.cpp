@@ -2,8 +2,11 @@
 //
 // Host-side duties: argument checks (before any HIP call), choice of the block
 // shape, the per-device cache of curve tables (built once per grid on the
-// device and kept), the per-device internal workspace for layer copies, and
-// the launches.  Nothing here computes any part of the product.
+// device and kept), the per-stream internal workspace for layer copies and
+// arrival counters, and the launches.  Nothing here computes any part of the
+// product.  No entry point synchronises the device or a stream: new curve
+// tables and workspaces are made stream-ordered (events, hipMallocAsync /
+// hipFreeAsync).
 #include <hip/hip_runtime.h>
 
 #include <map>
@@ -20,10 +23,28 @@ namespace {
 
 thread_local std::string g_last_error;
 
-struct DeviceState {
-  std::map<std::tuple<int, int, int>, int32_t*> tables;   // (gm, gn, order) -> device table
+// A curve table on the device, written by a kernel on the stream of the call
+// that first needed it; `ready` marks its completion for calls on other streams.
+struct Table {
+  int32_t* d = nullptr;
+  hipEvent_t ready = nullptr;
+  bool done = false;        // `ready` has been seen complete
+};
+
+// Library-owned memory of one stream: the layer copies of calls that pass no
+// workspace, and the arrival counters of fused reductions (kept zero between
+// launches).  Only work on that stream touches it, so calls on different
+// streams never share it; it grows stream-ordered.
+struct StreamMem {
   void* ws = nullptr;
   size_t ws_bytes = 0;
+  int32_t* counters = nullptr;
+  int64_t n_counters = 0;
+};
+
+struct DeviceState {
+  std::map<std::tuple<int, int, int>, Table> tables;   // (gm, gn, order) -> device table
+  std::map<hipStream_t, StreamMem> streams;
   int num_cus = 0;
   int occupancy[sfc::kNumTiles][2][2][2] = {};               // [tile][bf16 out][vec][fp8 in], 0 = unknown
 };
@@ -56,26 +77,93 @@ int device_state(DeviceState** out) {
   return SFC_OK;
 }
 
-// Curve table of a gm x gn grid on the current device, built on first use.
-// Must be called with g_mu held.
+// Curve table of a gm x gn grid on the current device.  The first call for a
+// grid allocates it and enqueues the generator on `stream` (no wait); a later
+// call on another stream waits for that kernel on the device, until the table
+// is known to be complete.  Must be called with g_mu held.
 int get_table(DeviceState& st, int gm, int gn, int order, hipStream_t stream, const int32_t** out) {
   auto key = std::make_tuple(gm, gn, order);
   auto it = st.tables.find(key);
   if (it != st.tables.end()) {
-    *out = it->second;
+    Table& t = it->second;
+    if (!t.done) {
+      hipError_t e = hipEventQuery(t.ready);
+      if (e == hipSuccess) {
+        t.done = true;
+      } else if (e == hipErrorNotReady) {
+        (void)hipGetLastError();   // not an error: do not leave it for the next check
+        e = hipStreamWaitEvent(stream, t.ready, 0);
+        if (e != hipSuccess) return hip_fail(e, "hipStreamWaitEvent(curve table)");
+      } else {
+        return hip_fail(e, "hipEventQuery(curve table)");
+      }
+    }
+    *out = t.d;
     return SFC_OK;
   }
-  int32_t* d = nullptr;
-  hipError_t e = hipMalloc(&d, sizeof(int32_t) * (size_t)gm * (size_t)gn);
+  Table t;
+  hipError_t e = hipMalloc(&t.d, sizeof(int32_t) * (size_t)gm * (size_t)gn);
   if (e != hipSuccess) return hip_fail(e, "hipMalloc(curve table)");
-  e = sfc::launch_sfc_order(gm, gn, order, d, stream);
-  if (e == hipSuccess) e = hipStreamSynchronize(stream);
+  e = sfc::launch_sfc_order(gm, gn, order, t.d, stream);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&t.ready, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventRecord(t.ready, stream);
   if (e != hipSuccess) {
-    (void)hipFree(d);
+    // the generator may be queued: the table is kept (never used) rather than freed under it
     return hip_fail(e, "curve table");
   }
-  st.tables[key] = d;
-  *out = d;
+  st.tables[key] = t;
+  *out = t.d;
+  return SFC_OK;
+}
+
+// At least `bytes` of layer workspace owned by `stream`.  A smaller buffer is
+// released stream-ordered (after the work already queued on the stream that
+// uses it) and a larger one allocated in stream order.  Must be called with
+// g_mu held.
+int stream_workspace(DeviceState& st, hipStream_t stream, size_t bytes, void** out) {
+  StreamMem& m = st.streams[stream];
+  if (m.ws_bytes < bytes) {
+    if (m.ws) {
+      hipError_t e = hipFreeAsync(m.ws, stream);
+      m.ws = nullptr;
+      m.ws_bytes = 0;
+      if (e != hipSuccess) return hip_fail(e, "hipFreeAsync(workspace)");
+    }
+    hipError_t e = hipMallocAsync(&m.ws, bytes, stream);
+    if (e != hipSuccess) {
+      m.ws = nullptr;
+      return hip_fail(e, "hipMallocAsync(workspace)");
+    }
+    m.ws_bytes = bytes;
+  }
+  *out = m.ws;
+  return SFC_OK;
+}
+
+// At least n arrival counters owned by `stream`, all zero when the next
+// launch on the stream starts (new ones are cleared by a fill kernel; the
+// fused reduction leaves every counter it used at zero).  Must be called with
+// g_mu held.
+int stream_counters(DeviceState& st, hipStream_t stream, int64_t n, int32_t** out) {
+  StreamMem& m = st.streams[stream];
+  if (m.n_counters < n) {
+    if (m.counters) {
+      hipError_t e = hipFreeAsync(m.counters, stream);
+      m.counters = nullptr;
+      m.n_counters = 0;
+      if (e != hipSuccess) return hip_fail(e, "hipFreeAsync(counters)");
+    }
+    const int64_t cap = n < 4096 ? 4096 : n;
+    hipError_t e = hipMallocAsync(reinterpret_cast<void**>(&m.counters), (size_t)cap * 4u, stream);
+    if (e != hipSuccess) {
+      m.counters = nullptr;
+      return hip_fail(e, "hipMallocAsync(counters)");
+    }
+    e = sfc::launch_fill_i32(m.counters, cap, 0, stream);
+    if (e != hipSuccess) return hip_fail(e, "counter fill");
+    m.n_counters = cap;
+  }
+  *out = m.counters;
   return SFC_OK;
 }
 
@@ -216,14 +304,20 @@ int plan_tail_split(DeviceState& st, const Plan& pl, int64_t M, int64_t N, int64
   return SFC_OK;
 }
 
-// One GEMM launch of plan pl into out (C, or the layer copies when pl.ce > 1).
-// Must be called with g_mu held.
-int launch_plan(DeviceState& st, const Plan& pl, int64_t M, int64_t N, int64_t K, const void* A, int64_t lda,
-                const void* B, int64_t ldb, void* out, int64_t ldo, int64_t layer_stride, bool out_bf16,
-                int order, int sched, hipStream_t stream, int f8) {
-  const int32_t* table = nullptr;
-  int rc = get_table(st, pl.gm, pl.gn, order, stream, &table);
-  if (rc != SFC_OK) return rc;
+// The fused reduction's part of a launch: C and the arrival counters (none:
+// the layer copies are summed by the separate reduction kernel).
+struct Fuse {
+  int32_t* counters = nullptr;
+  void* C = nullptr;
+  int64_t ldc = 0;
+  bool bf16 = false;
+};
+
+// One GEMM launch of plan pl into out (C, or the layer copies when pl.ce > 1),
+// blocks taken in the order of `table`.  Must be called with g_mu held.
+int launch_plan(const Plan& pl, const int32_t* table, int64_t M, int64_t N, int64_t K, const void* A,
+                int64_t lda, const void* B, int64_t ldb, void* out, int64_t ldo, int64_t layer_stride,
+                bool out_bf16, int sched, const Fuse& fu, hipStream_t stream, int f8) {
   sfc::GemmParams p;
   p.M = M; p.N = N; p.K = K;
   p.A = reinterpret_cast<const uint16_t*>(A); p.lda = lda;
@@ -235,15 +329,21 @@ int launch_plan(DeviceState& st, const Plan& pl, int64_t M, int64_t N, int64_t K
   p.nk = pl.nk;
   p.tasks = (int64_t)pl.gm * pl.gn * pl.ce;
   p.sched = sched;
-  p.pad_ = 0;
+  p.c_bf16 = fu.bf16 ? 1 : 0;
+  p.counters = fu.counters;
+  p.C = fu.C;
+  p.ldc = fu.ldc;
   hipError_t e = sfc::launch_gemm(pl.tile, out_bf16, pl.vec, p, pl.grid, stream, f8);
   if (e != hipSuccess) return hip_fail(e, "GEMM launch");
   return SFC_OK;
 }
 
+// How the layer copies of a call with c_eff > 1 are summed.
+enum Reduce { kReduceSeparate = 0, kReduceFused = 1 };
+
 int gemm_impl(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* B,
               int64_t ldb, void* C, int64_t ldc, int out_type, int ca_layers, int tile, int order,
-              int sched, void* ws, size_t ws_bytes, void* stream_ptr, int f8 = 0) {
+              int sched, void* ws, size_t ws_bytes, void* stream_ptr, int f8 = 0, int reduce = kReduceSeparate) {
   const sfc::Checked chk =
       f8 ? sfc::check_gemm_f8_args(M, N, K, A, lda, B, ldb, C, ldc, out_type, ca_layers, tile, order, sched, ws,
                                    ws_bytes)
@@ -269,6 +369,7 @@ int gemm_impl(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const
     rc = plan_tail_split(*st, pl, M, N, K, A, lda, B, ldb, ob, &sp);
     if (rc != SFC_OK) return rc;
   }
+  const Fuse none;
   if (sp.on) {
     Plan main = pl;
     main.gn -= sp.w;
@@ -276,43 +377,40 @@ int gemm_impl(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const
     const int64_t slots = (int64_t)st->num_cus * main.occ;
     main.grid = (int)(tasks < slots ? tasks : slots);
     const int64_t n1 = (int64_t)main.gn * main.bn;
-    rc = launch_plan(*st, main, M, n1, K, A, lda, B, ldb, C, ldc, 0, ob, order, sched, stream, 0);
+    const int32_t *t_main = nullptr, *t_strip = nullptr;
+    rc = get_table(*st, main.gm, main.gn, order, stream, &t_main);
+    if (rc == SFC_OK) rc = get_table(*st, sp.strip.gm, sp.strip.gn, order, stream, &t_strip);
+    if (rc != SFC_OK) return rc;
+    rc = launch_plan(main, t_main, M, n1, K, A, lda, B, ldb, C, ldc, 0, ob, sched, none, stream, 0);
     if (rc != SFC_OK) return rc;
     const size_t esz = ob ? 2 : 4;
-    return launch_plan(*st, sp.strip, M, N - n1, K, A, lda, static_cast<const uint16_t*>(B) + n1, ldb,
-                       static_cast<char*>(C) + (size_t)n1 * esz, ldc, 0, ob, order, sched, stream, 0);
+    return launch_plan(sp.strip, t_strip, M, N - n1, K, A, lda, static_cast<const uint16_t*>(B) + n1, ldb,
+                       static_cast<char*>(C) + (size_t)n1 * esz, ldc, 0, ob, sched, none, stream, 0);
   }
 
-  float* W = nullptr;
-  if (pl.ce > 1) {
-    const size_t need = (size_t)pl.ce * (size_t)M * (size_t)N * 4u;
-    if (ws) {
-      W = reinterpret_cast<float*>(ws);
-    } else {
-      if (st->ws_bytes < need) {
-        if (st->ws) {
-          // the old buffer may still be in use by queued work
-          hipError_t e = hipDeviceSynchronize();
-          if (e != hipSuccess) return hip_fail(e, "hipDeviceSynchronize(workspace)");
-          (void)hipFree(st->ws);
-          st->ws = nullptr;
-          st->ws_bytes = 0;
-        }
-        hipError_t e = hipMalloc(&st->ws, need);
-        if (e != hipSuccess) return hip_fail(e, "hipMalloc(workspace)");
-        st->ws_bytes = need;
-      }
-      W = reinterpret_cast<float*>(st->ws);
-    }
-  }
-
-  if (pl.ce > 1) rc = launch_plan(*st, pl, M, N, K, A, lda, B, ldb, W, N, M * N, false, order, sched, stream, f8);
-  else rc = launch_plan(*st, pl, M, N, K, A, lda, B, ldb, C, ldc, 0, ob, order, sched, stream, f8);
+  const int32_t* table = nullptr;
+  rc = get_table(*st, pl.gm, pl.gn, order, stream, &table);
   if (rc != SFC_OK) return rc;
-  if (pl.ce > 1) {
-    hipError_t e = sfc::launch_reduce(W, pl.ce, M, N, C, ldc, ob, stream);
-    if (e != hipSuccess) return hip_fail(e, "reduction launch");
+  if (pl.ce == 1) return launch_plan(pl, table, M, N, K, A, lda, B, ldb, C, ldc, 0, ob, sched, none, stream, f8);
+
+  // layer copies: the caller's workspace, or this stream's own
+  void* W = ws;
+  if (!W) {
+    rc = stream_workspace(*st, stream, (size_t)pl.ce * (size_t)M * (size_t)N * 4u, &W);
+    if (rc != SFC_OK) return rc;
   }
+  Fuse fu;
+  if (reduce == kReduceFused) {
+    rc = stream_counters(*st, stream, (int64_t)pl.gm * pl.gn, &fu.counters);
+    if (rc != SFC_OK) return rc;
+    fu.C = C;
+    fu.ldc = ldc;
+    fu.bf16 = ob;
+  }
+  rc = launch_plan(pl, table, M, N, K, A, lda, B, ldb, W, N, M * N, false, sched, fu, stream, f8);
+  if (rc != SFC_OK || reduce == kReduceFused) return rc;
+  hipError_t e = sfc::launch_reduce(static_cast<const float*>(W), pl.ce, M, N, C, ldc, ob, stream);
+  if (e != hipSuccess) return hip_fail(e, "reduction launch");
   return SFC_OK;
 }
 
@@ -349,6 +447,8 @@ int sfc_tile_order_ex(int gm, int gn, int order, int32_t* out_idx) {
   const int32_t* table = nullptr;
   rc = get_table(*st, gm, gn, order, nullptr, &table);
   if (rc != SFC_OK) return rc;
+  // a synchronous copy on the null stream: it follows the generator (get_table
+  // made the null stream wait for it if it was enqueued on another stream)
   hipError_t e = hipMemcpy(out_idx, table, sizeof(int32_t) * (size_t)gm * (size_t)gn,
                            hipMemcpyDeviceToHost);
   if (e != hipSuccess) return hip_fail(e, "hipMemcpy(curve table)");
@@ -380,6 +480,13 @@ int sfc_gemm_f8_fmt_ex(int64_t M, int64_t N, int64_t K, const void* A, int64_t l
     return set_error(SFC_ERR_INVALID_ARG, "unknown fp8 format");
   return gemm_impl(M, N, K, A, lda, B, ldb, C, ldc, out_type, ca_layers, tile, order, sched, ws,
                    ws_bytes, stream, 1 + a_format + 2 * b_format);
+}
+
+int sfc_gemm_fused_ex(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* B,
+                      int64_t ldb, void* C, int64_t ldc, int out_type, int ca_layers, int tile, int order,
+                      int sched, void* ws, size_t ws_bytes, void* stream) {
+  return gemm_impl(M, N, K, A, lda, B, ldb, C, ldc, out_type, ca_layers, tile, order, sched, ws,
+                   ws_bytes, stream, 0, kReduceFused);
 }
 
 int sfc_gemm(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* B, int64_t ldb,

@@ -34,7 +34,7 @@ SCHEDS = {"interleaved": 0, "block": 1, "interleaved_plain": 2}
 
 # Every symbol include/sfcgemm.h declares.
 EXPORTS = ["sfc_tile_order", "sfc_tile_order_ex", "sfc_gemm", "sfc_gemm_bf16out", "sfc_gemm_ws_size",
-           "sfc_gemm_ex", "sfc_gemm_f8_ex", "sfc_gemm_f8_fmt_ex", "sfc_gemm_plan", "sfc_gemm_model", "sfc_probe_mfma", "sfc_strerror",
+           "sfc_gemm_ex", "sfc_gemm_fused_ex", "sfc_gemm_f8_ex", "sfc_gemm_f8_fmt_ex", "sfc_gemm_plan", "sfc_gemm_model", "sfc_probe_mfma", "sfc_strerror",
            "sfc_last_error", "sfc_version"]
 
 
@@ -60,6 +60,8 @@ def _load() -> ctypes.CDLL:
     lib.sfc_gemm_bf16out.restype = i32
     lib.sfc_gemm_ex.argtypes = [i64, i64, i64, p, i64, p, i64, p, i64, i32, i32, i32, i32, i32, p, sz, p]
     lib.sfc_gemm_ex.restype = i32
+    lib.sfc_gemm_fused_ex.argtypes = [i64, i64, i64, p, i64, p, i64, p, i64, i32, i32, i32, i32, i32, p, sz, p]
+    lib.sfc_gemm_fused_ex.restype = i32
     lib.sfc_gemm_f8_ex.argtypes = [i64, i64, i64, p, i64, p, i64, p, i64, i32, i32, i32, i32, i32, p, sz, p]
     lib.sfc_gemm_f8_ex.restype = i32
     lib.sfc_gemm_f8_fmt_ex.argtypes = [i64, i64, i64, p, i64, p, i64, p, i64, i32, i32, i32, i32, i32, i32, i32, p,
@@ -152,30 +154,83 @@ def _stream_handle(stream) -> Optional[int]:
     return stream.cuda_stream
 
 
-def sfc_gemm_ex(A, B, C, ca_layers: int = 1, tile: str = "auto", order: str = "hilbert",
-                sched: str = "interleaved", workspace=None, stream=None) -> None:
-    """C = A @ B on the GPU.  A: (M, K) bf16, B: (K, N) bf16, C: (M, N) float32
-    or bfloat16 (the output type), all CUDA tensors with unit column stride."""
+def _operands(A, B, C, what: str, in_types, in_name: str, out_types):
+    """Checks shared by every GEMM wrapper, all made before the library is
+    called: A (M, K), B (K, N) and C (M, N) are 2-D tensors with unit column
+    stride and matching shapes, A and B hold `in_name` elements, C's dtype is
+    one of `out_types`, and all three live on the current CUDA device.
+    Returns (pa, lda, pb, ldb, pc, ldc, M, N, K, out_type)."""
     import torch
+    for t, n in ((A, "A"), (B, "B"), (C, "C")):
+        if not isinstance(t, torch.Tensor):
+            raise TypeError(f"{what}: {n} must be a torch.Tensor")
     pa, M, K, lda = _matrix(A, "A")
     pb, K2, N, ldb = _matrix(B, "B")
     pc, M2, N2, ldc = _matrix(C, "C")
     if K2 != K or M2 != M or N2 != N:
-        raise ValueError(f"shape mismatch: A {tuple(A.shape)} B {tuple(B.shape)} C {tuple(C.shape)}")
+        raise ValueError(f"{what}: shape mismatch: A {tuple(A.shape)} B {tuple(B.shape)} C {tuple(C.shape)}")
     for t, n in ((A, "A"), (B, "B")):
-        if t.dtype not in (torch.bfloat16, torch.int16, torch.uint16):
-            raise TypeError(f"{n} must hold bf16 patterns")
-    if C.dtype == torch.float32:
-        out = SFC_OUT_F32
-    elif C.dtype == torch.bfloat16:
-        out = SFC_OUT_BF16
-    else:
-        raise TypeError("C must be float32 or bfloat16")
-    ws_ptr, ws_bytes = (None, 0) if workspace is None else (workspace.data_ptr(),
-                                                            workspace.numel() * workspace.element_size())
+        if t.dtype not in in_types:
+            raise TypeError(f"{what}: {n} must hold {in_name} (got {t.dtype})")
+    if C.dtype not in out_types:
+        raise TypeError(f"{what}: C must be " + " or ".join(str(d).replace("torch.", "") for d in out_types)
+                        + f" (got {C.dtype})")
+    out = SFC_OUT_F32 if C.dtype == torch.float32 else SFC_OUT_BF16
+    for t, n in ((A, "A"), (B, "B"), (C, "C")):
+        if not t.is_cuda:
+            raise ValueError(f"{what}: {n} must be a CUDA tensor (got {t.device})")
+    dev = torch.cuda.current_device()
+    for t, n in ((A, "A"), (B, "B"), (C, "C")):
+        if t.device.index != dev:
+            raise ValueError(f"{what}: {n} is on {t.device}, the current device is cuda:{dev}")
+    return pa, lda, pb, ldb, pc, ldc, M, N, K, out
+
+
+def _bf16_types():
+    import torch
+    return (torch.bfloat16, torch.int16, torch.uint16)
+
+
+def _f8_types():
+    import torch
+    return (torch.uint8, torch.int8, torch.float8_e4m3fn, torch.float8_e5m2)
+
+
+def _out_types(*names):
+    import torch
+    return tuple(getattr(torch, n) for n in names)
+
+
+def _workspace(workspace):
+    if workspace is None:
+        return None, 0
+    if not workspace.is_cuda:
+        raise ValueError("workspace must be a CUDA tensor")
+    return workspace.data_ptr(), workspace.numel() * workspace.element_size()
+
+
+def sfc_gemm_ex(A, B, C, ca_layers: int = 1, tile: str = "auto", order: str = "hilbert",
+                sched: str = "interleaved", workspace=None, stream=None) -> None:
+    """C = A @ B on the GPU.  A: (M, K) bf16, B: (K, N) bf16, C: (M, N) float32
+    or bfloat16 (the output type), all CUDA tensors with unit column stride."""
+    pa, lda, pb, ldb, pc, ldc, M, N, K, out = _operands(A, B, C, "sfc_gemm_ex", _bf16_types(), "bf16 patterns",
+                                                        _out_types("float32", "bfloat16"))
+    ws_ptr, ws_bytes = _workspace(workspace)
     _check(lib.sfc_gemm_ex(M, N, K, pa, lda, pb, ldb, pc, ldc, out, ca_layers, TILES[tile],
                            ORDERS[order], SCHEDS[sched], ws_ptr, ws_bytes, _stream_handle(stream)),
            "sfc_gemm_ex")
+
+
+def sfc_gemm_fused_ex(A, B, C, ca_layers: int = 1, tile: str = "auto", order: str = "hilbert",
+                      sched: str = "interleaved", workspace=None, stream=None) -> None:
+    """As sfc_gemm_ex, with the sum of the layer copies done inside the GEMM
+    launch by the last workgroup to finish each block."""
+    pa, lda, pb, ldb, pc, ldc, M, N, K, out = _operands(A, B, C, "sfc_gemm_fused_ex", _bf16_types(),
+                                                        "bf16 patterns", _out_types("float32", "bfloat16"))
+    ws_ptr, ws_bytes = _workspace(workspace)
+    _check(lib.sfc_gemm_fused_ex(M, N, K, pa, lda, pb, ldb, pc, ldc, out, ca_layers, TILES[tile],
+                                 ORDERS[order], SCHEDS[sched], ws_ptr, ws_bytes, _stream_handle(stream)),
+           "sfc_gemm_fused_ex")
 
 
 FP8_FORMATS = {"e4m3": 0, "e5m2": 1}
@@ -189,24 +244,10 @@ def sfc_gemm_f8_ex(A, B, C, ca_layers: int = 1, tile: str = "auto", order: str =
     each in its format ("e4m3" or "e5m2"); C: (M, N) float32 or bfloat16, all
     with unit column stride.  Both formats E4M3 call sfc_gemm_f8_ex, any other
     pair sfc_gemm_f8_fmt_ex."""
-    import torch
-    pa, M, K, lda = _matrix(A, "A")
-    pb, K2, N, ldb = _matrix(B, "B")
-    pc, M2, N2, ldc = _matrix(C, "C")
-    if K2 != K or M2 != M or N2 != N:
-        raise ValueError(f"shape mismatch: A {tuple(A.shape)} B {tuple(B.shape)} C {tuple(C.shape)}")
-    for t, n in ((A, "A"), (B, "B")):
-        if t.dtype not in (torch.uint8, torch.int8, torch.float8_e4m3fn, torch.float8_e5m2):
-            raise TypeError(f"{n} must hold fp8 bytes")
+    pa, lda, pb, ldb, pc, ldc, M, N, K, out = _operands(A, B, C, "sfc_gemm_f8_ex", _f8_types(), "fp8 bytes",
+                                                        _out_types("float32", "bfloat16"))
     fa, fb = FP8_FORMATS[a_format], FP8_FORMATS[b_format]
-    if C.dtype == torch.float32:
-        out = SFC_OUT_F32
-    elif C.dtype == torch.bfloat16:
-        out = SFC_OUT_BF16
-    else:
-        raise TypeError("C must be float32 or bfloat16")
-    ws_ptr, ws_bytes = (None, 0) if workspace is None else (workspace.data_ptr(),
-                                                            workspace.numel() * workspace.element_size())
+    ws_ptr, ws_bytes = _workspace(workspace)
     if fa == 0 and fb == 0:
         _check(lib.sfc_gemm_f8_ex(M, N, K, pa, lda, pb, ldb, pc, ldc, out, ca_layers, TILES[tile],
                                   ORDERS[order], SCHEDS[sched], ws_ptr, ws_bytes, _stream_handle(stream)),
@@ -225,17 +266,15 @@ def to_device_u8(bits: np.ndarray, device="cuda"):
 
 def sfc_gemm(A, B, C, ca_layers: int = 1, stream=None) -> None:
     """C (float32) = A @ B with the default tile choice, curve order and schedule."""
-    pa, M, K, lda = _matrix(A, "A")
-    pb, _, N, ldb = _matrix(B, "B")
-    pc, _, _, ldc = _matrix(C, "C")
+    pa, lda, pb, ldb, pc, ldc, M, N, K, _ = _operands(A, B, C, "sfc_gemm", _bf16_types(), "bf16 patterns",
+                                                      _out_types("float32"))
     _check(lib.sfc_gemm(M, N, K, pa, lda, pb, ldb, pc, ldc, ca_layers, _stream_handle(stream)), "sfc_gemm")
 
 
 def sfc_gemm_bf16out(A, B, C, ca_layers: int = 1, stream=None) -> None:
     """C (bfloat16) = A @ B with the default tile choice, curve order and schedule."""
-    pa, M, K, lda = _matrix(A, "A")
-    pb, _, N, ldb = _matrix(B, "B")
-    pc, _, _, ldc = _matrix(C, "C")
+    pa, lda, pb, ldb, pc, ldc, M, N, K, _ = _operands(A, B, C, "sfc_gemm_bf16out", _bf16_types(),
+                                                      "bf16 patterns", _out_types("bfloat16"))
     _check(lib.sfc_gemm_bf16out(M, N, K, pa, lda, pb, ldb, pc, ldc, ca_layers, _stream_handle(stream)),
            "sfc_gemm_bf16out")
 

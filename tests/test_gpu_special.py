@@ -2,7 +2,8 @@
 operands propagate as IEEE arithmetic says (inf * 0 = NaN, inf - inf = NaN),
 element by element as the fp64 oracle gives them, for bf16 operands and for
 E5M2 operands (the fp8 format with infinities), with one layer and with the
-layer split; and two GEMMs enqueued on two streams at once each meet the bar."""
+layer split; and GEMMs enqueued on two streams at once, with one layer and with
+several (each stream with its own workspace), each meet the bar."""
 import numpy as np
 import pytest
 import torch
@@ -92,3 +93,36 @@ def test_two_streams_at_once():
         if out == "bf16":
             Cr = obf16.bf16_to_f64(obf16.f32_to_bf16_rne(Cr.astype(np.float32)))
         ocheck.assert_gemm_close(to_host(C), Cr, R, f"stream GEMM {Mx}x{Nx}x{Kx}")
+
+
+def test_two_streams_with_layers():
+    """sfc_gemm with c = 2 and with SFC_CA_AUTO (layers chosen by the model,
+    more than one on these K-dominant shapes), using the library's own
+    workspace, enqueued on two default-priority streams before either is waited
+    for; each stream also grows its workspace between its two calls.  Every
+    result meets the bar against the oracle."""
+    plan = [  # per stream: (M, N, K, ca_layers, seed), in enqueue order
+        [(256, 192, 8192, 2, 7401), (320, 256, 16384, 0, 7411)],
+        [(300, 200, 12288, 0, 7421), (512, 384, 6144, 2, 7431)],
+    ]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    jobs = []
+    for calls in plan:
+        for Mx, Nx, Kx, c, seed in calls:
+            A = draw(Mx, Kx, ("normal", 0.0, 1.0), seed)
+            B = draw(Kx, Nx, ("normal", 0.0, 1.0), seed + 1)
+            C = torch.full((Mx, Nx), float("nan"), dtype=torch.float32, device="cuda")
+            jobs.append((Mx, Nx, Kx, c, A, B, upload(A), upload(B), C))
+    torch.cuda.synchronize()
+    k = 0
+    for s, calls in zip(streams, plan):
+        for _ in calls:
+            Mx, Nx, Kx, c, _, _, dA, dB, C = jobs[k]
+            sg().sfc_gemm(dA, dB, C, ca_layers=c, stream=s)
+            k += 1
+    torch.cuda.synchronize()
+    for Mx, Nx, Kx, c, A, B, _, _, C in jobs:
+        if c == 0:
+            assert sg().sfc_gemm_plan(Mx, Nx, Kx, 0, "auto")["layers"] > 1
+        Cr, R = ogemm.gemm_ref_rows(A, B, Nx, Kx, Kx, Nx, M=Mx)
+        ocheck.assert_gemm_close(to_host(C), Cr, R, f"stream GEMM {Mx}x{Nx}x{Kx} c={c}")
