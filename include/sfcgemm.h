@@ -180,6 +180,34 @@ int sfc_gemm_fused_ex(int64_t M, int64_t N, int64_t K,
                       void *ws, size_t ws_bytes, void *stream);
 
 /*
+ * sfc_gemm_noalloc_ex -- sfc_gemm_ex for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc): the same kernels and results, bit for bit, with no
+ * allocation and no synchronisation in the call.  Instead of the library's
+ * per-stream workspace and cached curve tables it uses one static device
+ * array per GPU, held until the process ends: SFC_NOALLOC_WS_BYTES of fp32
+ * layer copies and two curve tables of SFC_NOALLOC_MAX_BLOCKS entries, which
+ * every call rewrites on `stream` (a small kernel before the GEMM).
+ *   Arguments and errors as for sfc_gemm_ex without a workspace, plus:
+ *   SFC_ERR_WORKSPACE   sfc_gemm_ws_size(M, N, K, ca_layers) exceeds
+ *                       SFC_NOALLOC_WS_BYTES (checked before any HIP call);
+ *   SFC_ERR_UNSUPPORTED the block grid has more than SFC_NOALLOC_MAX_BLOCKS
+ *                       blocks.
+ * Every call on a GPU uses that GPU's one array, whose contents are those the
+ * last call left: calls that overlap on one GPU (on different streams, or
+ * from different threads) race on it and must be ordered by the caller.  The
+ * first call on a device looks up the array's address (hipGetSymbolAddress).
+ */
+#define SFC_NOALLOC_WS_BYTES   ((size_t)64 << 20)   /* 64 MiB of layer copies */
+#define SFC_NOALLOC_MAX_BLOCKS (1 << 17)            /* blocks per curve table */
+int sfc_gemm_noalloc_ex(int64_t M, int64_t N, int64_t K,
+                        const void *A, int64_t lda,
+                        const void *B, int64_t ldb,
+                        void *C, int64_t ldc,
+                        int out_type, int ca_layers, int tile, int order, int sched,
+                        void *stream);
+
+/*
  * sfc_gemm_f8_ex -- C = A * B with 8-bit float operands (the paper leaves the
  * data type a parameter of the method, Section III.A): A and B hold OCP FP8
  * E4M3 bytes (1 sign, 4 exponent bits with bias 7, 3 mantissa bits; no

@@ -45,6 +45,7 @@ struct StreamMem {
 struct DeviceState {
   std::map<std::tuple<int, int, int>, Table> tables;   // (gm, gn, order) -> device table
   std::map<hipStream_t, StreamMem> streams;
+  char* scratch = nullptr;   // this device's copy of `scratch` (see sfc_gemm_noalloc_ex)
   int num_cus = 0;
   int occupancy[sfc::kNumTiles][2][2][2] = {};               // [tile][bf16 out][vec][fp8 in], 0 = unknown
 };
@@ -414,6 +415,99 @@ int gemm_impl(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const
   return SFC_OK;
 }
 
+// ---- the entry point that allocates nothing ---------------------------------------------
+// sfc_gemm_noalloc_ex keeps everything it needs beyond the caller's buffers in
+// this file-scope device array: the layer copies of a ca_layers > 1 call
+// (kNoAllocWsBytes) and the curve tables of its launches (two of at most
+// kNoAllocCells entries: the main grid and the half-height strip).  Each
+// device holds its own copy until the process ends.  In host code `scratch`
+// only names the array: its address on a device comes from
+// hipGetSymbolAddress, taken once per device with that device current.
+constexpr size_t kNoAllocWsBytes = SFC_NOALLOC_WS_BYTES;
+constexpr int64_t kNoAllocCells = SFC_NOALLOC_MAX_BLOCKS;
+constexpr size_t kNoAllocTableOffset = kNoAllocWsBytes;
+constexpr size_t kScratchBytes = kNoAllocWsBytes + 2 * (size_t)kNoAllocCells * 4;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+// The current device's address of `scratch`.  Must be called with g_mu held.
+int scratch_address(DeviceState& st, char** out) {
+  if (!st.scratch) {
+    void* ptr = nullptr;
+    hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    st.scratch = static_cast<char*>(ptr);
+  }
+  *out = st.scratch;
+  return SFC_OK;
+}
+
+int gemm_noalloc_impl(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* B, int64_t ldb,
+                      void* C, int64_t ldc, int out_type, int ca_layers, int tile, int order, int sched,
+                      void* stream_ptr) {
+  const sfc::Checked chk =
+      sfc::check_gemm_args(M, N, K, A, lda, B, ldb, C, ldc, out_type, ca_layers, tile, order, sched, nullptr, 0);
+  if (chk.code != SFC_OK) return set_error(chk.code, chk.msg);
+  if (M == 0 || N == 0) return SFC_OK;
+  // the layer copies must fit (for SFC_CA_AUTO: the largest count the model picks)
+  const size_t need = sfc::ws_size(M, N, K, ca_layers);
+  if (need > kNoAllocWsBytes)
+    return set_error(SFC_ERR_WORKSPACE, "sfc_gemm_noalloc_ex: the layer copies need " + std::to_string(need) +
+                                            " bytes; its workspace holds " + std::to_string(kNoAllocWsBytes));
+  hipStream_t stream = reinterpret_cast<hipStream_t>(stream_ptr);
+  const bool ob = out_type == SFC_OUT_BF16;
+
+  std::lock_guard<std::mutex> lock(g_mu);
+  DeviceState* st = nullptr;
+  int rc = device_state(&st);
+  if (rc != SFC_OK) return rc;
+  char* base = nullptr;
+  rc = scratch_address(*st, &base);
+  if (rc != SFC_OK) return rc;
+  int32_t* tables = reinterpret_cast<int32_t*>(base + kNoAllocTableOffset);
+  float* W = reinterpret_cast<float*>(base);
+
+  Plan pl;
+  rc = make_plan(*st, M, N, K, A, lda, B, ldb, ob, ca_layers, tile, &pl);
+  if (rc != SFC_OK) return rc;
+  Split sp;
+  if (tile == SFC_TILE_AUTO) {
+    rc = plan_tail_split(*st, pl, M, N, K, A, lda, B, ldb, ob, &sp);
+    if (rc != SFC_OK) return rc;
+  }
+  Plan main = pl;
+  if (sp.on) {
+    main.gn -= sp.w;
+    const int64_t tasks = (int64_t)main.gm * main.gn;
+    const int64_t slots = (int64_t)st->num_cus * main.occ;
+    main.grid = (int)(tasks < slots ? tasks : slots);
+  }
+  if ((int64_t)main.gm * main.gn > kNoAllocCells || (sp.on && (int64_t)sp.strip.gm * sp.strip.gn > kNoAllocCells))
+    return set_error(SFC_ERR_UNSUPPORTED, "sfc_gemm_noalloc_ex: more output blocks than its curve table holds (" +
+                                              std::to_string(kNoAllocCells) + ")");
+  // the curve tables are written on the stream for every call: the array
+  // keeps only what the last call left there
+  hipError_t e = sfc::launch_sfc_order(main.gm, main.gn, order, tables, stream);
+  if (e != hipSuccess) return hip_fail(e, "curve table");
+  const Fuse none;
+  if (sp.on) {
+    int32_t* t_strip = tables + kNoAllocCells;
+    e = sfc::launch_sfc_order(sp.strip.gm, sp.strip.gn, order, t_strip, stream);
+    if (e != hipSuccess) return hip_fail(e, "curve table");
+    const int64_t n1 = (int64_t)main.gn * main.bn;
+    rc = launch_plan(main, tables, M, n1, K, A, lda, B, ldb, C, ldc, 0, ob, sched, none, stream, 0);
+    if (rc != SFC_OK) return rc;
+    const size_t esz = ob ? 2 : 4;
+    return launch_plan(sp.strip, t_strip, M, N - n1, K, A, lda, static_cast<const uint16_t*>(B) + n1, ldb,
+                       static_cast<char*>(C) + (size_t)n1 * esz, ldc, 0, ob, sched, none, stream, 0);
+  }
+  if (pl.ce == 1) return launch_plan(pl, tables, M, N, K, A, lda, B, ldb, C, ldc, 0, ob, sched, none, stream, 0);
+  rc = launch_plan(pl, tables, M, N, K, A, lda, B, ldb, W, N, M * N, false, sched, none, stream, 0);
+  if (rc != SFC_OK) return rc;
+  e = sfc::launch_reduce(W, pl.ce, M, N, C, ldc, ob, stream);
+  if (e != hipSuccess) return hip_fail(e, "reduction launch");
+  return SFC_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -480,6 +574,12 @@ int sfc_gemm_f8_fmt_ex(int64_t M, int64_t N, int64_t K, const void* A, int64_t l
     return set_error(SFC_ERR_INVALID_ARG, "unknown fp8 format");
   return gemm_impl(M, N, K, A, lda, B, ldb, C, ldc, out_type, ca_layers, tile, order, sched, ws,
                    ws_bytes, stream, 1 + a_format + 2 * b_format);
+}
+
+int sfc_gemm_noalloc_ex(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* B,
+                        int64_t ldb, void* C, int64_t ldc, int out_type, int ca_layers, int tile, int order,
+                        int sched, void* stream) {
+  return gemm_noalloc_impl(M, N, K, A, lda, B, ldb, C, ldc, out_type, ca_layers, tile, order, sched, stream);
 }
 
 int sfc_gemm_fused_ex(int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* B,

@@ -34,7 +34,7 @@ SCHEDS = {"interleaved": 0, "block": 1, "interleaved_plain": 2}
 
 # Every symbol include/sfcgemm.h declares.
 EXPORTS = ["sfc_tile_order", "sfc_tile_order_ex", "sfc_gemm", "sfc_gemm_bf16out", "sfc_gemm_ws_size",
-           "sfc_gemm_ex", "sfc_gemm_fused_ex", "sfc_gemm_f8_ex", "sfc_gemm_f8_fmt_ex", "sfc_gemm_plan", "sfc_gemm_model", "sfc_probe_mfma", "sfc_strerror",
+           "sfc_gemm_ex", "sfc_gemm_fused_ex", "sfc_gemm_noalloc_ex", "sfc_gemm_f8_ex", "sfc_gemm_f8_fmt_ex", "sfc_gemm_plan", "sfc_gemm_model", "sfc_probe_mfma", "sfc_strerror",
            "sfc_last_error", "sfc_version"]
 
 
@@ -62,6 +62,8 @@ def _load() -> ctypes.CDLL:
     lib.sfc_gemm_ex.restype = i32
     lib.sfc_gemm_fused_ex.argtypes = [i64, i64, i64, p, i64, p, i64, p, i64, i32, i32, i32, i32, i32, p, sz, p]
     lib.sfc_gemm_fused_ex.restype = i32
+    lib.sfc_gemm_noalloc_ex.argtypes = [i64, i64, i64, p, i64, p, i64, p, i64, i32, i32, i32, i32, i32, p]
+    lib.sfc_gemm_noalloc_ex.restype = i32
     lib.sfc_gemm_f8_ex.argtypes = [i64, i64, i64, p, i64, p, i64, p, i64, i32, i32, i32, i32, i32, p, sz, p]
     lib.sfc_gemm_f8_ex.restype = i32
     lib.sfc_gemm_f8_fmt_ex.argtypes = [i64, i64, i64, p, i64, p, i64, p, i64, i32, i32, i32, i32, i32, i32, i32, p,
@@ -231,6 +233,23 @@ def sfc_gemm_fused_ex(A, B, C, ca_layers: int = 1, tile: str = "auto", order: st
     _check(lib.sfc_gemm_fused_ex(M, N, K, pa, lda, pb, ldb, pc, ldc, out, ca_layers, TILES[tile],
                                  ORDERS[order], SCHEDS[sched], ws_ptr, ws_bytes, _stream_handle(stream)),
            "sfc_gemm_fused_ex")
+
+
+NOALLOC_WS_BYTES = 64 << 20
+NOALLOC_MAX_BLOCKS = 1 << 17
+
+
+def sfc_gemm_noalloc_ex(A, B, C, ca_layers: int = 1, tile: str = "auto", order: str = "hilbert",
+                        sched: str = "interleaved", stream=None) -> None:
+    """As sfc_gemm_ex without a workspace argument, for callers that cannot
+    allocate: the library's static per-GPU array holds the layer copies (at
+    most NOALLOC_WS_BYTES) and the curve tables.  Calls that overlap on one GPU
+    race on that array."""
+    pa, lda, pb, ldb, pc, ldc, M, N, K, out = _operands(A, B, C, "sfc_gemm_noalloc_ex", _bf16_types(),
+                                                        "bf16 patterns", _out_types("float32", "bfloat16"))
+    _check(lib.sfc_gemm_noalloc_ex(M, N, K, pa, lda, pb, ldb, pc, ldc, out, ca_layers, TILES[tile],
+                                   ORDERS[order], SCHEDS[sched], _stream_handle(stream)),
+           "sfc_gemm_noalloc_ex")
 
 
 FP8_FORMATS = {"e4m3": 0, "e5m2": 1}

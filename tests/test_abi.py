@@ -164,3 +164,32 @@ def test_f8_format_codes_validated(sg):
         assert "format" in sg.last_error()
     # valid codes reach the other checks: a misaligned A is still rejected
     assert sg.lib.sfc_gemm_f8_fmt_ex(64, 64, 64, 4096 + 8, 64, 8192, 64, 16384, 64, F32, 1, 1, *tail) == -2
+
+
+def call_noalloc(sg, **kw):
+    a = dict(GOOD)
+    a.update(kw)
+    return sg.lib.sfc_gemm_noalloc_ex(a["M"], a["N"], a["K"], a["A"], a["lda"], a["B"], a["ldb"], a["C"], a["ldc"],
+                                      a["out"], a["c"], a["tile"], a["order"], a["sched"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(M=-1), -1), (dict(lda=63), -1), (dict(C=None), -1), (dict(c=65), -1), (dict(tile=5), -1),
+    (dict(A=4097), -2),
+    # layer copies beyond the static workspace (64 MiB): 2 x 2048 x 4096 x 4 B = 64 MiB fits, one more row does not
+    (dict(M=2049, N=4096, ldc=4096, ldb=4096, K=128, lda=128, c=2), -3),
+    (dict(M=1024, N=1024, ldc=1024, ldb=1024, K=65536, lda=65536, c=17), -3),
+    # SFC_CA_AUTO is checked at the largest count the model picks (16)
+    (dict(M=1025, N=1024, ldc=1024, ldb=1024, K=65536, lda=65536, c=0), -3),
+])
+def test_noalloc_rejected_before_any_launch(sg, kw, code):
+    assert call_noalloc(sg, **kw) == code
+    assert sg.last_error() != ""
+    if code == -3:
+        assert "workspace holds" in sg.last_error()
+
+
+def test_noalloc_empty_output_is_a_noop(sg):
+    assert call_noalloc(sg, M=0, C=None, A=None) == 0
+    assert call_noalloc(sg, N=0, C=None, B=None) == 0
+    assert sg.NOALLOC_WS_BYTES == 64 << 20
