@@ -68,22 +68,26 @@ def parse():
                     help="run the kernel of one workload (or fp8_square8192) K times and exit")
     ap.add_argument("--sweep", action="store_true", help="also run the 125-shape sweep")
     ap.add_argument("--sweep-reps", type=int, default=3, help="cold repetitions per autotune candidate")
+    ap.add_argument("--tune-reps", type=int, default=3,
+                    help="cold repetitions per candidate of the per-workload autotune")
+    ap.add_argument("--no-autotune", action="store_true", help="skip the per-workload model-vs-autotune check")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="with --only: also run a plain device copy of MIB MiB (counter calibration)")
     return ap.parse_args()
 
 
-def traffic_record():
-    """HBM bytes per launch from committed rocprofv3 counter runs, valid only
+def counter_record():
+    """Per-launch figures of the headline kernel from committed rocprofv3
+    counter runs (HBM bytes, shader cycles per XCD, MFMA busy), valid only
     while the GEMM kernel source is the one the counters were taken on."""
     try:
         rec = json.load(open(TRAFFIC_FILE))
     except (OSError, ValueError):
-        return None
+        return {}
     sha = hashlib.sha256(open(GEMM_SRC, "rb").read()).hexdigest()
     if rec.get("kernel_src_sha256") != sha:
-        return None
-    return rec.get("hbm_bytes_per_launch")
+        return {}
+    return rec
 
 
 def roofline_tflops(M, N, K, out_bytes):
@@ -180,9 +184,9 @@ def main():
     stream = torch.cuda.current_stream()
     W = {w.name: w for w in workloads()}
 
-    def run_once(dA, dB, C, w, c, sched=None):
-        sg.sfc_gemm_ex(dA, dB, C, ca_layers=c, tile=w.tile, order=args.order, sched=sched or args.sched,
-                       stream=stream)
+    def run_once(dA, dB, C, w, c, sched=None, tile=None, fused=False):
+        f = sg.sfc_gemm_fused_ex if fused else sg.sfc_gemm_ex
+        f(dA, dB, C, ca_layers=c, tile=tile or w.tile, order=args.order, sched=sched or args.sched, stream=stream)
 
     def prepare(g):
         A, B = g.operands()
@@ -368,33 +372,69 @@ def main():
             for x in wl.gemms:
                 pm = sg.sfc_gemm_plan(x.M, x.N, x.K, 0, wl.tile)
                 entry["model_choice"].append({"tile": f"{pm['BM']}x{pm['BN']}", "ca_layers": pm["layers"]})
-            def timed(c, sched=None):
+            ops = [prepare(gg)[2:] for gg in wl.gemms]
+
+            def cold_ms(gi, c, reps, sched=None, tile=None, fused=False):
+                """Mean of `reps` cold calls (512 MiB flush before each, untimed)."""
+                a, b, cc = ops[gi]
+                ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                      for _ in range(reps)]
+                for s, e in ev:
+                    flush.zero_()
+                    s.record(stream)
+                    run_once(a, b, cc, wl, c, sched, tile, fused)
+                    e.record(stream)
+                torch.cuda.synchronize()
+                return sum(s.elapsed_time(e) for s, e in ev) / reps
+
+            def timed(c, sched=None, tile=None, fused=False):
                 cold_t = warm_t = 0.0
-                for gg in wl.gemms:
-                    _, _, a, b, cc = prepare(gg)
+                for gi in range(len(wl.gemms)):
+                    a, b, cc = ops[gi]
                     for _ in range(3):
-                        run_once(a, b, cc, wl, c, sched)
+                        run_once(a, b, cc, wl, c, sched, tile, fused)
                     torch.cuda.synchronize()
-                    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-                          for _ in range(args.reps)]
-                    for s, e in ev:                           # cold: caches flushed, untimed
-                        flush.zero_()
-                        s.record(stream)
-                        run_once(a, b, cc, wl, c, sched)
-                        e.record(stream)
-                    torch.cuda.synchronize()
-                    cold_t += sum(s.elapsed_time(e) for s, e in ev) / args.reps
+                    cold_t += cold_ms(gi, c, args.reps, sched, tile, fused)
                     s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
                     s.record(stream)
                     for _ in range(args.reps):
-                        run_once(a, b, cc, wl, c, sched)
+                        run_once(a, b, cc, wl, c, sched, tile, fused)
                     e.record(stream)
                     torch.cuda.synchronize()
                     warm_t += s.elapsed_time(e) / args.reps
-                    del a, b, cc
                 return {"cold_ms": round(cold_t, 4), "warm_ms": round(warm_t, 4),
                         "tflops_cold": round(wl.flops / (cold_t * 1e-3) / 1e12, 2),
                         "tflops_warm": round(wl.flops / (warm_t * 1e-3) / 1e12, 2)}
+
+            def autotune():
+                """The model's choice (SFC_TILE_AUTO, SFC_CA_AUTO) against the best of
+                the four block shapes x ca_layers in {1, 2, 4, 8, 16} (layer copies
+                up to 2 GiB), each timed cold, per GEMM: the GPU counterpart of
+                Section III.C's knob prediction checked against autotuning."""
+                best_t = model_t = 0.0
+                rows = []
+                for gi, x in enumerate(wl.gemms):
+                    a, b, cc = ops[gi]
+                    cands = []
+                    for t in ("128x128", "256x128", "128x256", "256x256"):
+                        for c in (1, 2, 4, 8, 16):
+                            if c > 1 and c * x.M * x.N * 4 > (2 << 30):
+                                continue
+                            run_once(a, b, cc, wl, c, None, t)
+                            cands.append((cold_ms(gi, c, args.tune_reps, None, t), t, c))
+                    run_once(a, b, cc, wl, 0, None, "auto")
+                    mt = cold_ms(gi, 0, args.tune_reps, None, "auto")
+                    bt = min(cands)
+                    pm = sg.sfc_gemm_plan(x.M, x.N, x.K, 0, "auto")
+                    rows.append({"gemm": [x.M, x.N, x.K],
+                                 "model": {"tile": f"{pm['BM']}x{pm['BN']}", "ca_layers": pm["layers"],
+                                           "cold_ms": round(mt, 4)},
+                                 "best": {"tile": bt[1], "ca_layers": bt[2], "cold_ms": round(bt[0], 4)},
+                                 "candidates": len(cands)})
+                    best_t += bt[0]
+                    model_t += mt
+                return {"protocol": f"each candidate: mean of {args.tune_reps} cold calls", "per_gemm": rows,
+                        "model_over_best": round(best_t / model_t, 4)}
 
             per_c = {}
             for c in wl.ca_layers:
@@ -407,6 +447,20 @@ def main():
                 entry["layer_placement"] = {"chiplet_aware": per_c["auto"],
                                             "hardware_order": timed(0, "interleaved_plain")}
                 log(f"[bench] {name} placement: {entry['layer_placement']}")
+                # the layer copies summed inside the GEMM launch (sfc_gemm_fused_ex)
+                # against the separate reduction kernel, per layer count
+                entry["fused_reduction"] = {("auto" if c == 0 else c): timed(c, fused=True)
+                                            for c in wl.ca_layers if c != 1}
+                log(f"[bench] {name} fused reduction: {entry['fused_reduction']}")
+            if wl.tile != "auto":
+                # the configuration pins the block shape and one layer; the
+                # library's own choice on the same GEMM, for comparison
+                entry["model_choice_timed"] = timed(0, tile="auto")
+                log(f"[bench] {name} at the model's choice: {entry['model_choice_timed']}")
+            if not args.no_autotune:
+                entry["model_vs_autotune"] = autotune()
+                log(f"[bench] {name} model vs autotune: {entry['model_vs_autotune']['model_over_best']}")
+            del ops
             best_c = max(per_c, key=lambda k: per_c[k]["tflops_cold"])
             best = per_c[best_c]
             # roofline of the workload: min(MFMA peak, OI x HBM) per GEMM with its
@@ -427,9 +481,13 @@ def main():
         del flush
         whm = whm_num / whm_den
         best_shape = max(v["tflops"] for v in table.values())
+        tuned = [v["model_vs_autotune"]["model_over_best"] for v in table.values() if "model_vs_autotune" in v]
         table = {"protocol": f"mean of {args.reps} cold reps (512 MiB flush between), best ca_layers",
                  "shapes": table, "whm_tflops": round(whm, 2),
                  "whm_over_best_shape": round(whm / best_shape, 4)}
+        if tuned:
+            table["model_over_autotune_mean"] = round(sum(tuned) / len(tuned), 4)
+            table["model_over_autotune_min"] = round(min(tuned), 4)
 
     sweep = run_sweep(args, sg, torch, stream, dev) if args.sweep else None
 
@@ -447,11 +505,38 @@ def main():
         t = time.perf_counter()
         ogemm.gemm_ref_rows(A_host, B_host, g.N, g.K, g.K, g.N, row0=0, nrows=rows)
         dt = time.perf_counter() - t
+        cpu_model = "unknown"
+        try:
+            for ln in open("/proc/cpuinfo"):
+                if ln.startswith("model name"):
+                    cpu_model = ln.split(":", 1)[1].strip()
+                    break
+        except OSError:
+            pass
         cpu = {"value": round(2.0 * rows * g.N * g.K / dt / 1e12, 6), "unit": "TFLOP/s",
-               "cores": threads, "kind": "oracle",
+               "cores": threads, "kind": "oracle", "cpu_model": cpu_model,
+               "host_cpus": os.cpu_count(),
                "sample": f"rows 0..{rows - 1} of the {g.M}x{g.N}x{g.K} GEMM "
                          f"({rows}x{g.N} outputs, fp64, {dt:.1f} s)"}
 
+    counters = counter_record()
+    # The kernel's shader cycles per launch do not depend on the box or the
+    # operands (committed counter runs); its duration follows the clock the
+    # board holds under load.  Cycles / duration is that clock, and 4096 flop
+    # per CU per clock at that clock is the MFMA ceiling of this very run.
+    clock = None
+    if counters.get("cycles_per_xcd_per_launch"):
+        ghz = counters["cycles_per_xcd_per_launch"] / (kern_ms * 1e-3) / 1e9
+        ceiling = PEAK_BF16_TFLOPS * ghz / 2.4
+        clock = {"ghz_implied": round(ghz, 3), "mfma_ceiling_at_that_clock": round(ceiling, 1),
+                 "frac_of_that_ceiling": round(achieved / ceiling, 4),
+                 "cycles_per_xcd_per_launch": counters["cycles_per_xcd_per_launch"],
+                 "mfma_busy_per_clock": counters.get("mfma_busy")}
+    cold_c2 = None
+    if table is not None:
+        e2 = table["shapes"][HEADLINE]
+        cold_c2 = {"protocol": table["protocol"], "tflops": e2["tflops"],
+                   "frac_of_mfma_peak": e2["frac_of_mfma_peak"], "tflops_warm_10": e2["tflops_warm"]}
     line = {
         "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
@@ -463,11 +548,14 @@ def main():
                    "dist": "A, B ~ N(0,1) rounded to bf16"},
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                     "traffic": traffic_record(), "kernel": "sfc_gemm_kernel<256,256,bf16 out>",
+                     "traffic": counters.get("hbm_bytes_per_launch"),
+                     "kernel": "sfc_gemm_kernel<256,256,bf16 out>",
                      "kernel_ms": round(kern_ms, 4),
                      "mfma_probe": probe,
                      "frac_of_probe_random": round(achieved / probe["random_operands"]["tflops"], 4),
-                     "same_kernel_constant_operands": constant},
+                     "same_kernel_constant_operands": constant,
+                     "loaded_clock": clock},
+        "headline_cold": cold_c2,
         "cpu_baseline": cpu,
         "library_same_workload": library,
         "fp8_square8192": fp8,
