@@ -71,6 +71,10 @@ def parse():
     ap.add_argument("--tune-reps", type=int, default=3,
                     help="cold repetitions per candidate of the per-workload autotune")
     ap.add_argument("--no-autotune", action="store_true", help="skip the per-workload model-vs-autotune check")
+    ap.add_argument("--only-layers", type=int, default=None, help="with --only: ca_layers (0: the model's)")
+    ap.add_argument("--only-tile", default=None, help="with --only: block shape (default: the workload's)")
+    ap.add_argument("--cold", action="store_true", help="with --only: flush 512 MiB before every call")
+    ap.add_argument("--fused", action="store_true", help="with --only: sum the layer copies inside the GEMM")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="with --only: also run a plain device copy of MIB MiB (counter calibration)")
     return ap.parse_args()
@@ -206,13 +210,23 @@ def main():
         log(f"[bench] ran fp8_square8192 {args.steps} times")
         return
     if args.only:
+        # one workload's GEMMs (each called --steps times, in turn), for
+        # profilers: --only-layers picks the layer count (default: the last of
+        # the workload's list), --only-tile the block shape, --cold flushes
+        # 512 MiB before every call, --fused sums the layer copies in the GEMM
         ow = W[args.only]
-        og = ow.gemms[0]
-        _, _, oA, oB, oC = prepare(og)
-        for _ in range(args.steps):
-            run_once(oA, oB, oC, ow, ow.ca_layers[-1])
-        torch.cuda.synchronize()
-        log(f"[bench] ran {args.only} {args.steps} times")
+        c_only = ow.ca_layers[-1] if args.only_layers is None else args.only_layers
+        flush = torch.empty(512 * 1024 * 1024 // 4, dtype=torch.float32, device=dev) if args.cold else None
+        for og in ow.gemms:
+            _, _, oA, oB, oC = prepare(og)
+            for _ in range(args.steps):
+                if flush is not None:
+                    flush.zero_()
+                run_once(oA, oB, oC, ow, c_only, tile=args.only_tile, fused=args.fused)
+            torch.cuda.synchronize()
+            log(f"[bench] ran {args.only} {og.M}x{og.N}x{og.K} ca_layers={c_only} order={args.order} "
+                f"{'cold ' if args.cold else ''}{args.steps} times")
+            del oA, oB, oC
         if args.calibrate_copy:
             n = args.calibrate_copy * 1024 * 1024 // 4
             src = torch.ones(n, dtype=torch.float32, device=dev)
