@@ -9,8 +9,11 @@ the critical path, adds the reads/writes of C and, for 2.5D/3D runs, of the C
 copies, and takes the decomposition with the smallest time (Section III.C,
 second option).  The reading for this GPU (listed in the design doc):
 
-* a core is a CU; it runs ``occ`` persistent workgroups, each of which gets
-  1/occ of the CU's MFMA rate (gamma = occ / (flops per clock x rate));
+* a core is a CU; it holds up to ``occ`` persistent workgroups; a workgroup
+  gets 1/w of its CU's MFMA rate (gamma = w / (flops per clock x rate)), where
+  w = min(occ, ceil(active / CUs)) is the number that actually share a CU: the
+  dispatcher spreads a grid over the CUs before it doubles up (and a grid of at
+  most one 128x128 block per CU runs a one-per-CU kernel);
 * one BRGEMM is one 64-deep K block of one task (BM x BN output block):
   G = 2*BM*BN*64 flops, S_A = BM*64*2 and S_B = 64*BN*2 bytes;
 * fast memory is an XCD's L2, slow memory is HBM.  The ``active`` tasks in
@@ -33,9 +36,10 @@ The calibration numbers are MI355X measurements (achieved MFMA rate per CU and
 per block shape, loaded HBM bytes per clock, launch cost).
 
 Parity: pinned in tests/test_oracle_model.py (Eq. 1 evaluated by hand on a
-compute-bound and a memory-bound block, two whole estimates written out by
-hand, the M <-> N symmetry, the K-dominant configuration of Section IV needing
-layers while a large square does not, ties).
+compute-bound and a memory-bound block, three whole estimates written out by
+hand -- one of a grid smaller than the machine, where a workgroup has its CU
+to itself -- the M <-> N symmetry, the K-dominant configuration of Section IV
+needing layers while a large square does not, ties).
 """
 from __future__ import annotations
 
@@ -70,7 +74,8 @@ def estimate(M: int, N: int, K: int, out_bytes: int, num_cus: int, occ: Dict[Tup
     blocks = -(-nK // c)
     active = min(tasks, slots)
     G = 2.0 * BM * BN * BK
-    gamma = o / (FLOPS_PER_CLK_CU * RATE[shape])
+    w = min(o, max(1, -(-active // num_cus)))
+    gamma = w / (FLOPS_PER_CLK_CU * RATE[shape])
     patch = max(1.0, active / XCDS)
     beta = active / HBM_BYTES_PER_CLK
     t_blk = brgemm_clk(G, gamma, beta / math.sqrt(patch), BM * BK * 2.0, BK * BN * 2.0)

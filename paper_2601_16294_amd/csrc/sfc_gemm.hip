@@ -268,14 +268,22 @@ constexpr int stage_k() { return F8 ? 64 : kSK; }
 __device__ __forceinline__ int b_swz8(int k) { return (k & 7) << 1; }
 
 // The loads of block b+D are issued during block b (prefetch depth D): the A
-// ring has D+1 block slots, the B ring 2D stage slots.  D = 3 where the LDS
-// holds that at the same occupancy (128x256: exactly 160 KiB), else 2.
-template <int BM, int BN, int NW, int F8>
+// ring has D+1 block slots, the B ring 2D stage slots.  By default D = 3 where
+// the LDS holds that at the same occupancy (128x256: exactly 160 KiB), else 2.
+// 128x128 blocks run two workgroups per CU at D = 2 (80 KiB each); when a grid
+// has no more blocks than CUs that occupancy buys nothing, and a kernel with
+// D = 4 (144 KiB, one workgroup per CU) keeps twice the blocks in flight, which
+// is what a short grid with long K is bound by (the latency of its operand
+// stream).
+template <int BM, int BN>
+constexpr int default_depth() { return (BM == 128 && BN == 256) ? 3 : 2; }
+
+template <int BM, int BN, int NW, int F8, int DEPTH = default_depth<BM, BN>()>
 struct Ring {
   static constexpr int A_BLK = BM * kBK;                 // elements of one A block
   static constexpr int B_STG = kSK * BN;                 // elements of one B stage
   static constexpr int A_BYTES = A_BLK * 2, B_BYTES = B_STG * 2;
-  static constexpr int D = (BM == 128 && BN == 256) ? 3 : 2;
+  static constexpr int D = DEPTH;
   static constexpr int NA = D + 1, NB = 2 * D;           // A block slots, B stage slots
   static constexpr int B_OFF = NA * A_BYTES;             // byte offset of the B slots
   static constexpr int APB = A_BYTES / 1024 / NW;        // A loads per wave per block
@@ -286,7 +294,7 @@ struct Ring {
   static_assert(APB % 4 == 0 && (BPW == 2 || BPW == 4), "tile shape");
   static_assert(ELEMS * 2 <= 160 * 1024, "LDS of one CU");
   static_assert(IN_FLIGHT <= 63, "vmcnt range");
-  static_assert(D == 2 || D == 3, "ring depth");
+  static_assert(D >= 2 && D <= 4, "ring depth");
 };
 
 // Two loads sharing M0: LDS M0+OFF+16*lane and M0+OFF+1024+16*lane.
@@ -642,7 +650,7 @@ __device__ __forceinline__ void group_dma(const SlotDma& d0, const SlotDma& d1, 
   ((void)(P::dma_group(o) == g ? (step_dma<BM, BN, NW, F8, OP, o>(d0, d1, L), 0) : 0), ...);
 }
 
-template <int BM, int BN, int NW, int F8, int OP, int g, typename X>
+template <int BM, int BN, int NW, int F8, int D, int OP, int g, typename X>
 __device__ __forceinline__ void ring_group(Acc<BM, BN, NW, F8>& acc, const Frags<BM, BN, NW, F8>& cur, Frags<BM, BN, NW, F8>& nxt,
                                            uint32_t a_base, uint32_t b_slot, const uint32_t* b_rd,
                                            BReads<BM, BN, NW, F8>& br, const SlotDma& d0, const SlotDma& d1,
@@ -661,7 +669,7 @@ __device__ __forceinline__ void ring_group(Acc<BM, BN, NW, F8>& acc, const Frags
     // every wave's reads issued in the A step are done (among them the last
     // reads of the B slot this step loads into, and of the A slot the next A
     // step loads into)
-    wait_vmem_at_most<Ring<BM, BN, NW, F8>::IN_FLIGHT>();
+    wait_vmem_at_most<Ring<BM, BN, NW, F8, D>::IN_FLIGHT>();
     wait_lds_all();
     __syncthreads();
   }
@@ -671,12 +679,12 @@ __device__ __forceinline__ void ring_group(Acc<BM, BN, NW, F8>& acc, const Frags
   __builtin_amdgcn_sched_barrier(0);
 }
 
-template <int BM, int BN, int NW, int F8, int OP, typename X, int... g>
+template <int BM, int BN, int NW, int F8, int D, int OP, typename X, int... g>
 __device__ __forceinline__ void ring_groups(Acc<BM, BN, NW, F8>& acc, const Frags<BM, BN, NW, F8>& cur, Frags<BM, BN, NW, F8>& nxt,
                                             uint32_t a_base, uint32_t b_slot, const uint32_t* b_rd,
                                             BReads<BM, BN, NW, F8>& br, const SlotDma& d0, const SlotDma& d1,
                                             const RingLanes<BM, BN, NW, F8>& L, X& ex, std::integer_sequence<int, g...>) {
-  (ring_group<BM, BN, NW, F8, OP, g>(acc, cur, nxt, a_base, b_slot, b_rd, br, d0, d1, L, ex), ...);
+  (ring_group<BM, BN, NW, F8, D, OP, g>(acc, cur, nxt, a_base, b_slot, b_rd, br, d0, d1, L, ex), ...);
 }
 
 // One 32-deep step with a fixed instruction order (the plan above): MFMAs of
@@ -685,7 +693,7 @@ __device__ __forceinline__ void ring_groups(Acc<BM, BN, NW, F8>& acc, const Frag
 // (ex.operator()<g>() runs in group g).  The groups are generated as
 // straight-line code (a loop this long is not always unrolled, and the
 // accumulators must stay in registers).
-template <int BM, int BN, int NW, int F8, int OP, typename X>
+template <int BM, int BN, int NW, int F8, int D, int OP, typename X>
 __device__ __forceinline__ void ring_step(Acc<BM, BN, NW, F8>& acc, const Frags<BM, BN, NW, F8>& cur, Frags<BM, BN, NW, F8>& nxt,
                                           uint32_t a_base, uint32_t b_slot, const ReadOffsets<BM, BN, NW, F8>& o,
                                           const SlotDma& d0, const SlotDma& d1, const RingLanes<BM, BN, NW, F8>& L,
@@ -693,7 +701,7 @@ __device__ __forceinline__ void ring_step(Acc<BM, BN, NW, F8>& acc, const Frags<
   using T = Tile<BM, BN, NW, F8>;
   BReads<BM, BN, NW, F8> br;
   br.a_d = o.a_d;
-  ring_groups<BM, BN, NW, F8, OP>(acc, cur, nxt, a_base, b_slot, o.b_rd, br, d0, d1, L, ex,
+  ring_groups<BM, BN, NW, F8, D, OP>(acc, cur, nxt, a_base, b_slot, o.b_rd, br, d0, d1, L, ex,
                           std::make_integer_sequence<int, T::FM * T::FN>{});
 }
 
@@ -740,15 +748,14 @@ __device__ __forceinline__ uint32_t b_stage_limit(const RingAddr& ra, int x) {
 // outside the B descriptors' ranges and read zeros; A block nb-1 is loaded with
 // its lanes past K masked (selects on the first groups of the step that issues
 // those loads, or in the prologue when nb <= D).
-template <int BM, int BN, int NW, int F8>
+template <int BM, int BN, int NW, int F8, int D>
 __device__ __forceinline__ void main_loop_ring(const RingAddr& ra, int nb, int64_t kin_last,
                                                const ReadOffsets<BM, BN, NW, F8>& o, RingLanes<BM, BN, NW, F8>& L, int lane,
                                                Acc<BM, BN, NW, F8>& acc) {
-  using R = Ring<BM, BN, NW, F8>;
+  using R = Ring<BM, BN, NW, F8, D>;
   using T = Tile<BM, BN, NW, F8>;
   using P1 = StepPlan<BM, BN, NW, F8, 1>;
   using P2 = StepPlan<BM, BN, NW, F8, 2>;
-  constexpr int D = R::D;
   constexpr uint32_t BB = (uint32_t)R::B_BYTES;
   const int wave = ra.wave;
   const bool masked = kin_last < block_k<F8>();
@@ -820,8 +827,8 @@ __device__ __forceinline__ void main_loop_ring(const RingAddr& ra, int nb, int64
   const int mask_b = masked ? nb - 1 - D : -1;
 
   // scalar state of block b
-  // A slots of blocks b, b+1, b+2 (and b+3 for depth 3)
-  uint32_t la0 = 0, la1 = R::A_BYTES, la2 = 2 * R::A_BYTES, la3 = 3 * R::A_BYTES;
+  // A slots of blocks b, b+1, .., b+D
+  uint32_t la0 = 0, la1 = R::A_BYTES, la2 = 2 * R::A_BYTES, la3 = 3 * R::A_BYTES, la4 = 4 * R::A_BYTES;
   uint32_t sb = 0, lb1 = BB, lb2 = 2 * BB;  // B slots of stages x0 (and x0+2D), x0+1 (and x0+2D+1), x0+2
   uint64_t a_nx = ra.a0 + D * kBK * 2;      // A block b+D
   uint64_t b_nx = ra.b0 + 2 * D * ra.b_step; // B stage x0+2D
@@ -832,7 +839,7 @@ __device__ __forceinline__ void main_loop_ring(const RingAddr& ra, int nb, int64
   uint32_t lim0, lim1;
   uint64_t b_nx1;
   for (int b = 0; b < nb; ++b) {
-    ring_step<BM, BN, NW, F8, 1>(acc, f0, f1, ra.lds0 + la0 + o.a_rd[1], lb1, o, da, da, L, [&]<int g>() {
+    ring_step<BM, BN, NW, F8, D, 1>(acc, f0, f1, ra.lds0 + la0 + o.a_rd[1], lb1, o, da, da, L, [&]<int g>() {
       if constexpr (g < R::APB) {
         if (mnow && mk[g]) L.a_voff[g] = kOobOffset;
       }
@@ -846,16 +853,20 @@ __device__ __forceinline__ void main_loop_ring(const RingAddr& ra, int nb, int64
       if constexpr (g == P1::stage_group(4, 6)) b_nx1 = b_nx + ra.b_step;
       if constexpr (g == P1::stage_group(5, 6)) db1.rsrc = make_rsrc_addr(b_nx1, lim1);
     });
-    ring_step<BM, BN, NW, F8, 2>(acc, f1, f0, ra.lds0 + la1 + o.a_rd[0], lb2, o, db0, db1, L, [&]<int g>() {
+    ring_step<BM, BN, NW, F8, D, 2>(acc, f1, f0, ra.lds0 + la1 + o.a_rd[0], lb2, o, db0, db1, L, [&]<int g>() {
       if constexpr (g == P2::stage_group(0, 5)) {
         const uint32_t t = la0;
         la0 = la1;
         la1 = la2;
         if constexpr (D == 2) {
           la2 = t;
-        } else {
+        } else if constexpr (D == 3) {
           la2 = la3;
           la3 = t;
+        } else {
+          la2 = la3;
+          la3 = la4;
+          la4 = t;
         }
       }
       if constexpr (g == P2::stage_group(1, 5)) {
@@ -875,7 +886,7 @@ __device__ __forceinline__ void main_loop_ring(const RingAddr& ra, int nb, int64
       }
       if constexpr (g == P2::stage_group(3, 5)) {
         da.rsrc = make_rsrc_addr(a_nx, b + 1 + D < nb ? (uint32_t)kOobOffset : 0u);
-        da.m0 = a_m0w + (D == 2 ? la2 : la3);
+        da.m0 = a_m0w + (D == 2 ? la2 : D == 3 ? la3 : la4);
       }
       if constexpr (g == P2::stage_group(4, 5)) {
         b_nx += 2 * ra.b_step;
@@ -1373,13 +1384,13 @@ __device__ __forceinline__ void fused_finish(const GemmParams& p, int cell, int6
   if (tid == 0) __hip_atomic_store(p.counters + cell, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-template <int BM, int BN, int NW, int F8, bool OUT_BF16, bool VEC>
+template <int BM, int BN, int NW, int F8, bool OUT_BF16, bool VEC, int D = default_depth<BM, BN>()>
 __global__ __launch_bounds__(NW * 64, 1) void sfc_gemm_kernel(GemmParams p) {
   using T = Tile<BM, BN, NW, F8>;
   static_assert(T::A_CH >= 1 && T::B_CH >= 1, "tile too small for the workgroup");
   static_assert(!F8 || VEC, "fp8 operands take the fast path only");
   // fast path: the rings of A block and B stage slots; general path: two 64-deep blocks
-  constexpr int kSmem = VEC ? Ring<BM, BN, NW, F8>::ELEMS : 2 * (T::A_ELEMS + T::B_ELEMS);
+  constexpr int kSmem = VEC ? Ring<BM, BN, NW, F8, D>::ELEMS : 2 * (T::A_ELEMS + T::B_ELEMS);
   __shared__ __attribute__((aligned(16))) uint16_t smem[kSmem];
 
   const int tid = threadIdx.x;
@@ -1387,7 +1398,7 @@ __global__ __launch_bounds__(NW * 64, 1) void sfc_gemm_kernel(GemmParams p) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / T::WGN, wn = wave % T::WGN;
   ReadOffsets<BM, BN, NW, F8> ro;
-  if constexpr (VEC) read_offsets<BM, BN, NW, F8>(wm, wn, lane, lds_addr(smem) + (uint32_t)Ring<BM, BN, NW, F8>::B_OFF, ro);
+  if constexpr (VEC) read_offsets<BM, BN, NW, F8>(wm, wn, lane, lds_addr(smem) + (uint32_t)Ring<BM, BN, NW, F8, D>::B_OFF, ro);
 
   const int P = gridDim.x;
   // SFC_SCHED_INTERLEAVED_PLAIN keeps the hardware order (comparison only)
@@ -1459,7 +1470,7 @@ __global__ __launch_bounds__(NW * 64, 1) void sfc_gemm_kernel(GemmParams p) {
         }
         ra.lds0 = lds_addr(smem);
         ra.wave = wave;
-        main_loop_ring<BM, BN, NW, F8>(ra, kt1 - kt0, p.K - (int64_t)(kt1 - 1) * block_k<F8>(), ro, L, lane_t,
+        main_loop_ring<BM, BN, NW, F8, D>(ra, kt1 - kt0, p.K - (int64_t)(kt1 - 1) * block_k<F8>(), ro, L, lane_t,
                                        acc);
       } else if constexpr (!F8) {
         main_loop_staged<BM, BN, NW, F8>(p, smem, m0, n0, kt0, kt1, tid, acc);
@@ -1496,9 +1507,9 @@ __global__ __launch_bounds__(NW * 64, 1) void sfc_gemm_kernel(GemmParams p) {
 // but read 1.5x the LDS bytes and ran at a lower clock for the same time.)
 constexpr int kWaves = 4;
 
-template <int BM, int BN, int NW, int F8, bool OB, bool VEC>
+template <int BM, int BN, int NW, int F8, bool OB, bool VEC, int D = default_depth<BM, BN>()>
 static const void* kernel_ptr() {
-  return reinterpret_cast<const void*>(&sfc_gemm_kernel<BM, BN, NW, F8, OB, VEC>);
+  return reinterpret_cast<const void*>(&sfc_gemm_kernel<BM, BN, NW, F8, OB, VEC, D>);
 }
 
 // fp8 operands (f8 = 1 + a + 2b, a and b the formats of A and B: 0 OCP E4M3,
@@ -1516,7 +1527,13 @@ static const void* select_kernel_f8(int tile, bool ob, int f8) {
 #undef SFC_K8
 }
 
-static const void* select_kernel(int tile, bool ob, bool vec) {
+// deep: the 4-deep ring of 128x128 blocks (fast path), for grids of at most
+// one block per CU.
+static const void* select_kernel(int tile, bool ob, bool vec, bool deep) {
+  if (deep) {
+    if (tile != kT128x128 || !vec) return nullptr;
+    return ob ? kernel_ptr<128, 128, kWaves, 0, true, true, 4>() : kernel_ptr<128, 128, kWaves, 0, false, true, 4>();
+  }
 #define SFC_K(BM_, BN_, NW_)                                                                   \
   return ob ? (vec ? kernel_ptr<BM_, BN_, NW_, 0, true, true>() : kernel_ptr<BM_, BN_, 4, 0, true, false>()) \
             : (vec ? kernel_ptr<BM_, BN_, NW_, 0, false, true>() : kernel_ptr<BM_, BN_, 4, 0, false, false>())
@@ -1533,16 +1550,16 @@ static const void* select_kernel(int tile, bool ob, bool vec) {
 static int threads_of(int, bool) { return kWaves * 64; }
 
 hipError_t launch_gemm(int tile, bool out_bf16, bool vec, const GemmParams& p, int grid,
-                       hipStream_t stream, int f8) {
-  const void* k = f8 ? select_kernel_f8(tile, out_bf16, f8) : select_kernel(tile, out_bf16, vec);
+                       hipStream_t stream, int f8, bool deep) {
+  const void* k = f8 ? select_kernel_f8(tile, out_bf16, f8) : select_kernel(tile, out_bf16, vec, deep);
   if (!k) return hipErrorInvalidValue;
   GemmParams local = p;
   void* args[] = {&local};
   return hipLaunchKernel(k, dim3(grid), dim3(threads_of(tile, vec)), args, 0, stream);
 }
 
-hipError_t gemm_occupancy(int tile, bool out_bf16, bool vec, int* blocks_per_cu, int f8) {
-  const void* k = f8 ? select_kernel_f8(tile, out_bf16, f8) : select_kernel(tile, out_bf16, vec);
+hipError_t gemm_occupancy(int tile, bool out_bf16, bool vec, int* blocks_per_cu, int f8, bool deep) {
+  const void* k = f8 ? select_kernel_f8(tile, out_bf16, f8) : select_kernel(tile, out_bf16, vec, deep);
   if (!k) return hipErrorInvalidValue;
   return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks_per_cu, k, threads_of(tile, vec), 0);
 }

@@ -24,8 +24,14 @@ double candidate_clk(int64_t M, int64_t N, int64_t nk, int out_bytes, int num_cu
   // one BRGEMM (64-deep block): G flops, panels S_A + S_B bytes
   const double g = 2.0 * (double)bm * (double)bn * 64.0;
   const double s_ab = 2.0 * 64.0 * (double)(bm + bn);
-  // gamma: a workgroup gets 1/occ of its CU's MFMA rate
-  const double t_compute = g * (double)occ / (k.flops_per_clk_cu * k.rate[t]);
+  // gamma: a workgroup gets 1/w of its CU's MFMA rate, w the workgroups that
+  // share the CU: the dispatcher spreads a grid over the CUs before it puts a
+  // second workgroup on one (and a grid of at most one 128x128 block per CU
+  // runs the one-per-CU kernel)
+  int64_t w = cdiv(active, num_cus);
+  if (w > occ) w = occ;
+  if (w < 1) w = 1;
+  const double t_compute = g * (double)w / (k.flops_per_clk_cu * k.rate[t]);
   // beta: HBM shared by the active workgroups; each panel read once per XCD patch
   double patch = (double)active / (double)k.xcds;
   if (patch < 1.0) patch = 1.0;

@@ -42,10 +42,12 @@ hipError_t launch_sfc_order(int gm, int gn, int order, int32_t* dev_out, hipStre
 // (needs 16-byte aligned A and B, lda, ldb, K and N multiples of 8).
 // f8 = 0: bf16 operands; f8 = 1 + a + 2b: A and B hold OCP fp8 bytes of format a
 // and b (0 E4M3, 1 E5M2; lda, ldb in elements = bytes); 256x256 only.
+// deep = true: 128x128 blocks on the fast path with a 4-deep ring (one
+// workgroup per CU), for grids of at most one block per CU.
 hipError_t launch_gemm(int tile, bool out_bf16, bool vec, const GemmParams& p, int grid,
-                       hipStream_t stream, int f8 = 0);
+                       hipStream_t stream, int f8 = 0, bool deep = false);
 // Workgroups of the given kernel variant that fit on one CU.
-hipError_t gemm_occupancy(int tile, bool out_bf16, bool vec, int* blocks_per_cu, int f8 = 0);
+hipError_t gemm_occupancy(int tile, bool out_bf16, bool vec, int* blocks_per_cu, int f8 = 0, bool deep = false);
 
 // p[0 .. n) = v (a fill kernel: usable where a memset node is not wanted).
 hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t stream);

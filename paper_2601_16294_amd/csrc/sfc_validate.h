@@ -111,6 +111,13 @@ inline int strip_columns(int gm, int gn, int64_t slots, int64_t half_rows, int64
   return (int)w;
 }
 
+// Whether a launch takes the 4-deep ring of 128x128 blocks: the fast path,
+// bf16 operands, 128x128 blocks and no more tasks (blocks x layers) than CUs,
+// so that one workgroup per CU (instead of two) loses nothing.
+inline bool deep_ring(int tile_128x128, bool vec, int f8, int64_t tasks, int64_t num_cus) {
+  return tile_128x128 && vec && f8 == 0 && tasks > 0 && tasks <= num_cus;
+}
+
 // 16-byte loads are legal when every row starts 16-byte aligned and the K and
 // N extents end on whole 8-element chunks.
 inline bool vector_loads_ok(const void* A, int64_t lda, const void* B, int64_t ldb, int64_t K,

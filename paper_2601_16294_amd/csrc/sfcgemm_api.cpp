@@ -48,6 +48,7 @@ struct DeviceState {
   char* scratch = nullptr;   // this device's copy of `scratch` (see sfc_gemm_noalloc_ex)
   int num_cus = 0;
   int occupancy[sfc::kNumTiles][2][2][2] = {};               // [tile][bf16 out][vec][fp8 in], 0 = unknown
+  int occupancy_deep[2] = {};                                  // 4-deep 128x128 ring, [bf16 out]
 };
 
 std::mutex g_mu;
@@ -168,11 +169,11 @@ int stream_counters(DeviceState& st, hipStream_t stream, int64_t n, int32_t** ou
   return SFC_OK;
 }
 
-int get_occupancy(DeviceState& st, int tile, bool ob, bool vec, int* occ, int f8 = 0) {
-  int& o = st.occupancy[tile][ob][vec][f8 != 0];
+int get_occupancy(DeviceState& st, int tile, bool ob, bool vec, int* occ, int f8 = 0, bool deep = false) {
+  int& o = deep ? st.occupancy_deep[ob] : st.occupancy[tile][ob][vec][f8 != 0];
   if (o == 0) {
     int v = 0;
-    hipError_t e = sfc::gemm_occupancy(tile, ob, vec, &v, f8);
+    hipError_t e = sfc::gemm_occupancy(tile, ob, vec, &v, f8, deep);
     if (e != hipSuccess) return hip_fail(e, "occupancy query");
     o = v < 1 ? 1 : v;
   }
@@ -193,6 +194,7 @@ int tile_from_api(int t) {
 struct Plan {
   int tile, bm, bn, gm, gn, ce, nk, grid, occ;
   bool vec;
+  bool deep = false;   // 128x128 blocks with the 4-deep ring (one workgroup per CU)
 };
 
 int make_plan(DeviceState& st, int64_t M, int64_t N, int64_t K, const void* A, int64_t lda,
@@ -251,9 +253,11 @@ int make_plan(DeviceState& st, int64_t M, int64_t N, int64_t K, const void* A, i
   pl->nk = (int)(K > 0 ? sfc::ceil_div(K, sfc::kBK) : 0);
   // layer copies are fp32 whatever the output type
   const bool kernel_bf16 = ob && pl->ce == 1;
-  rc = get_occupancy(st, pl->tile, kernel_bf16, pl->vec, &pl->occ);
-  if (rc != SFC_OK) return rc;
   const int64_t tasks = (int64_t)pl->gm * pl->gn * pl->ce;
+  // a grid of at most one 128x128 block per CU runs the deep-ring kernel
+  pl->deep = sfc::deep_ring(pl->tile == sfc::kT128x128, pl->vec, 0, tasks, st.num_cus);
+  rc = get_occupancy(st, pl->tile, kernel_bf16, pl->vec, &pl->occ, 0, pl->deep);
+  if (rc != SFC_OK) return rc;
   int64_t slots = (int64_t)st.num_cus * pl->occ;
   pl->grid = (int)(tasks < slots ? tasks : slots);
   return SFC_OK;
@@ -334,7 +338,7 @@ int launch_plan(const Plan& pl, const int32_t* table, int64_t M, int64_t N, int6
   p.counters = fu.counters;
   p.C = fu.C;
   p.ldc = fu.ldc;
-  hipError_t e = sfc::launch_gemm(pl.tile, out_bf16, pl.vec, p, pl.grid, stream, f8);
+  hipError_t e = sfc::launch_gemm(pl.tile, out_bf16, pl.vec, p, pl.grid, stream, f8, pl.deep);
   if (e != hipSuccess) return hip_fail(e, "GEMM launch");
   return SFC_OK;
 }

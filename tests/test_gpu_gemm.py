@@ -224,7 +224,9 @@ def test_auto_layers_match_oracle(M, N, K, out):
     ocheck.assert_gemm_close(C, Cr, R, f"auto {M}x{N}x{K} {out}")
     plan = sg().sfc_gemm_plan(M, N, K, 0, "auto")
     cus = torch.cuda.get_device_properties(0).multi_processor_count
-    occ = tuple(sg().sfc_gemm_plan(M, N, K, 1, t)["per_cu"] for t in TILES)
+    # the model weighs the block shapes at their full-grid occupancy (a grid of
+    # at most one 128x128 block per CU runs a one-per-CU kernel instead)
+    occ = tuple(sg().sfc_gemm_plan(8192, 8192, 64, 1, t)["per_cu"] for t in TILES)
     model = sg().sfc_gemm_model(M, N, K, out="f32", ca_layers=0, num_cus=cus, occupancy=occ)
     assert (f"{plan['BM']}x{plan['BN']}", plan["layers"]) == (model["tile"], model["layers"])
     assert plan["layers"] > 1
@@ -253,3 +255,34 @@ def test_bf16_store_paths_by_alignment(tile):
         pad = to_host(buf[offset:].view(M, ldc))[:, N:]
         assert np.isnan(pad).all(), (tile, offset, ldc)
         assert np.isnan(to_host(buf[:offset])).all()
+
+
+@pytest.mark.parametrize("K,out", [(2048, "f32"), (2000, "bf16")])
+def test_deep_ring_matches_two_per_cu_kernel(K, out):
+    """128x128 grids of at most one block per CU run the 4-deep ring kernel (one
+    workgroup per CU), larger ones the 2-deep ring (two per CU).  The two run the
+    same MFMA sequence per element, so the top-left 1024x1024 of a 4096x4096
+    product (1024 blocks: 2-deep) equals the 1024x1024 product of the same rows
+    and columns (64 blocks: 4-deep) bit for bit; both meet the bar on sampled
+    rows.  K = 2000 ends in a masked block."""
+    Mb, Ms = 4096, 1024
+    A = draw(Mb, K, U, 1500 + K)
+    B = draw(K, Mb, U, 1501 + K)
+    dA, dB = upload(A), upload(B)
+    dtype = torch.float32 if out == "f32" else torch.bfloat16
+    Cb = torch.full((Mb, Mb), float("nan"), dtype=dtype, device="cuda")
+    Cs = torch.full((Ms, Ms), float("nan"), dtype=dtype, device="cuda")
+    sg().sfc_gemm_ex(dA, dB, Cb, tile="128x128")
+    sg().sfc_gemm_ex(dA[:Ms], dB[:, :Ms].contiguous(), Cs, tile="128x128")
+    torch.cuda.synchronize()
+    assert sg().sfc_gemm_plan(Ms, Ms, K, 1, "128x128")["per_cu"] == 1
+    assert sg().sfc_gemm_plan(Mb, Mb, K, 1, "128x128")["per_cu"] == 2
+    assert np.array_equal(raw_bits(Cb)[:Ms, :Ms], raw_bits(Cs))
+    rows = [0, 127, 128, 640, 1023, 1024, 2047, 4095]
+    Cr, R = ogemm.gemm_ref_rows(np.ascontiguousarray(A[rows]), B, Mb, K, K, Mb, M=len(rows))
+    if out == "bf16":
+        Cr = obf16.bf16_to_f64(obf16.f32_to_bf16_rne(Cr.astype(np.float32)))
+    ocheck.assert_gemm_close(to_host(Cb)[rows], Cr, R, f"128x128 two per CU K={K} {out}")
+    small = [r for r in rows if r < Ms]
+    ocheck.assert_gemm_close(to_host(Cs)[small], Cr[:len(small), :Ms], R[:len(small), :Ms],
+                             f"128x128 deep ring K={K} {out}")

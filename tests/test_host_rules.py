@@ -1,4 +1,5 @@
-"""Host-side planning rules that need no GPU, compiled with g++ straight from
+"""Host-side planning rules that need no GPU (the half-height strip, the
+deep-ring kernel choice), compiled with g++ straight from
 the library's header-only checks (paper_2601_16294_amd/csrc/sfc_validate.h)."""
 import os
 import subprocess
@@ -66,3 +67,43 @@ def test_strip_leaves_whole_rounds(harness):
         assert gm * (gn - w) <= (T // S) * S
         assert hr * w <= hs
         assert 0 < T % S <= S // 2
+
+
+DEEP = r'''
+#include <stdio.h>
+#include <stdlib.h>
+#include "sfc_validate.h"
+int main(int argc, char** argv) {
+  for (int i = 1; i + 4 < argc; i += 5)
+    printf("%d\n", (int)sfc::deep_ring(atoi(argv[i]), atoi(argv[i + 1]) != 0, atoi(argv[i + 2]), atoll(argv[i + 3]),
+                                       atoll(argv[i + 4])));
+  return 0;
+}
+'''
+
+
+@pytest.fixture(scope="module")
+def deep_harness(tmp_path_factory):
+    d = tmp_path_factory.mktemp("deep")
+    src, exe = d / "d.cpp", d / "d"
+    src.write_text(DEEP)
+    subprocess.run(["g++", "-std=c++17", "-O1", f"-I{ROOT}/include", f"-I{ROOT}/paper_2601_16294_amd/csrc",
+                    str(src), "-o", str(exe)], check=True)
+    return str(exe)
+
+
+def test_deep_ring_rule(deep_harness):
+    # (128x128 blocks?, fast path?, fp8?, tasks, CUs) -> the 4-deep ring kernel
+    cases = {
+        (1, 1, 0, 16, 256): 1,      # 512^3 at 128x128: 16 blocks on 256 CUs
+        (1, 1, 0, 256, 256): 1,     # exactly one block per CU
+        (1, 1, 0, 257, 256): 0,     # more blocks than CUs: two per CU at the 2-deep ring
+        (1, 1, 0, 1320, 256): 0,
+        (0, 1, 0, 16, 256): 0,      # other block shapes fill the LDS already
+        (1, 0, 0, 16, 256): 0,      # element-load path
+        (1, 1, 1, 16, 256): 0,      # fp8 operands run 256x256 blocks
+        (1, 1, 0, 0, 256): 0,
+    }
+    args = [str(v) for c in cases for v in c]
+    out = subprocess.run([deep_harness] + args, capture_output=True, text=True, check=True).stdout.split()
+    assert [int(x) for x in out] == list(cases.values())

@@ -90,3 +90,29 @@ def test_worked_estimate_memory_bound():
     occ = {(128, 128): 2, (256, 128): 1, (128, 256): 1, (256, 256): 1}
     clk, _ = om.estimate(8192, 8192, 8192, 4, 4096, occ, (128, 256), 1)
     assert clk == pytest.approx(316783.38, rel=1e-8)
+
+
+def test_worked_estimate_grid_smaller_than_the_machine():
+    # 512 x 512 x 512, fp32 out, 128x128 blocks, 1 layer, 256 CUs, 2 workgroups
+    # per CU possible: 4*4 = 16 tasks, 1 round, 8 K blocks each.  16 workgroups
+    # on 256 CUs have a CU each (w = min(2, ceil(16/256)) = 1):
+    # block: 2,097,152 flops / (3031.04 * 0.60 = 1818.624) = 1153.15315 clk
+    # (panels 32,768 B * 16/3500 / sqrt(16/8) = 105.92 clk: compute-bound);
+    # 8 blocks = 9225.2252 clk; C 512*512*4 B / 3500 = 299.5931 clk; 1 launch.
+    # Total 19,524.8184 clk.  Charged half a CU (w = 2), the same block would
+    # take 2306.3 clk and the grid 28,749.7.
+    occ = {(128, 128): 2, (256, 128): 1, (128, 256): 1, (256, 256): 1}
+    clk, pad = om.estimate(512, 512, 512, 4, 256, occ, (128, 128), 1)
+    assert clk == pytest.approx(19524.8184, rel=1e-8)
+    assert pad == 16 * 128 * 128
+    # 128x256 blocks: 8 tasks of 4,194,304 flops / (3031.04 * 0.86) = 1609.05 clk
+    # per block: 10000 + 8 * 1609.05 + 299.59 = 23,172.0 clk -- slower, so the
+    # model takes 128x128 here (the measured faster shape of this GEMM)
+    clk2, _ = om.estimate(512, 512, 512, 4, 256, occ, (128, 256), 1)
+    assert clk2 == pytest.approx(23172.0004, rel=1e-8)
+    shape, c, _ = om.choose(512, 512, 512, out_bytes=4, occ=occ)
+    assert shape == (128, 128) and c == 1
+    # with more blocks than CUs two share a CU again
+    clk3, _ = om.estimate(4096, 4096, 512, 4, 256, occ, (128, 128), 1)
+    blk = 2097152 * 2 / 1818.624
+    assert clk3 == pytest.approx(10000 + 2 * 8 * max(blk, 512 / 3500 * 32768 / 8) + 4096 * 4096 * 4 / 3500, rel=1e-9)

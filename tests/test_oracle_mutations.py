@@ -101,7 +101,8 @@ MODEL_SRC = open(os.path.join(ROOT, "oracle", "model.py")).read()
 MODEL_MUTANTS = {
     "no_patch_sharing": ("t_blk = brgemm_clk(G, gamma, beta / math.sqrt(patch),", "t_blk = brgemm_clk(G, gamma, beta,"),
     "panel_a_uses_bn": ("BM * BK * 2.0, BK * BN * 2.0)", "BN * BK * 2.0, BK * BN * 2.0)"),
-    "gamma_ignores_occupancy": ("gamma = o / (FLOPS_PER_CLK_CU * RATE[shape])", "gamma = 1 / (FLOPS_PER_CLK_CU * RATE[shape])"),
+    "gamma_ignores_occupancy": ("gamma = w / (FLOPS_PER_CLK_CU * RATE[shape])", "gamma = 1 / (FLOPS_PER_CLK_CU * RATE[shape])"),
+    "sharing_ignores_grid_size": ("w = min(o, max(1, -(-active // num_cus)))", "w = o"),
     "copies_not_read_back": ("2 * c * M * N * 4 + M * N * out_bytes", "c * M * N * 4 + M * N * out_bytes"),
     "no_reduction_launch": ("launches = 1 if c == 1 else 2", "launches = 1"),
     "blocks_not_split": ("blocks = -(-nK // c)", "blocks = nK"),
@@ -147,6 +148,13 @@ def _model_pins(mod):
     clk, _ = mod.estimate(8192, 8192, 8192, 4, 4096, occ, (128, 256), 1)
     if abs(clk - 316783.38) > 316783.38 * 1e-8:
         fails.append("memory-bound worked estimate")
+    clk, _ = mod.estimate(512, 512, 512, 4, 256, occ, (128, 128), 1)
+    if abs(clk - 19524.8184) > 19524.8184 * 1e-8:
+        fails.append("small-grid worked estimate")
+    clk, _ = mod.estimate(4096, 4096, 512, 4, 256, occ, (128, 128), 1)
+    want = 10000 + 2 * 8 * max(2097152 * 2 / 1818.624, 512 / 3500 * 32768 / 8) + 4096 * 4096 * 4 / 3500
+    if abs(clk - want) > want * 1e-9:
+        fails.append("shared-CU worked estimate")
     return fails
 
 
