@@ -68,12 +68,15 @@ def parse():
                     help="run the kernel of one workload (or fp8_square8192) K times and exit")
     ap.add_argument("--sweep", action="store_true", help="also run the 125-shape sweep")
     ap.add_argument("--sweep-reps", type=int, default=3, help="cold repetitions per autotune candidate")
-    ap.add_argument("--tune-reps", type=int, default=3,
+    ap.add_argument("--tune-reps", type=int, default=5,
                     help="cold repetitions per candidate of the per-workload autotune")
     ap.add_argument("--no-autotune", action="store_true", help="skip the per-workload model-vs-autotune check")
     ap.add_argument("--only-layers", type=int, default=None, help="with --only: ca_layers (0: the model's)")
     ap.add_argument("--only-tile", default=None, help="with --only: block shape (default: the workload's)")
-    ap.add_argument("--cold", action="store_true", help="with --only: flush 512 MiB before every call")
+    ap.add_argument("--warm-clock-ms", type=float, default=200.0,
+                    help="back-to-back calls of a workload before it is timed (sweep shapes: a quarter)")
+    ap.add_argument("--cold", action="store_true",
+                    help="with --only: take the calls in rotation over >= 1 GiB of operand copies")
     ap.add_argument("--fused", action="store_true", help="with --only: sum the layer copies inside the GEMM")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="with --only: also run a plain device copy of MIB MiB (counter calibration)")
@@ -101,12 +104,69 @@ def roofline_tflops(M, N, K, out_bytes):
     return ("hbm", hbm) if hbm < PEAK_BF16_TFLOPS else ("mfma", PEAK_BF16_TFLOPS)
 
 
+def warm_clock(torch, stream, fn, min_ms):
+    """Run fn back to back for at least min_ms of wall time and return the
+    time per call of the first and of the last batch (HIP events).  A GPU that
+    sat idle while the host drew a workload's inputs runs its first tens of
+    milliseconds of work at a lower clock; the cold protocol clears the caches
+    between repetitions, it is not meant to time that clock ramp."""
+    t0 = time.perf_counter()
+    first = last = None
+    while True:
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record(stream)
+        for _ in range(4):
+            fn()
+        e.record(stream)
+        torch.cuda.synchronize()
+        last = s.elapsed_time(e) / 4
+        if first is None:
+            first = last
+        if (time.perf_counter() - t0) * 1e3 >= min_ms:
+            return round(first, 4), round(last, 4)
+
+
+ROTATION_BYTES = 1 << 30
+
+
+class ColdSets:
+    """The cold protocol of Section IV.A: copies of one GEMM's A, B and C,
+    enough of them (at least 2, together at least 1 GiB: past the 256 MiB
+    Infinity Cache and the 8 x 4 MiB of L2) that a call taken in rotation
+    finds none of its operands in a cache.  Nothing runs between the calls but
+    the other copies' GEMMs (no flush kernel, whose dirty lines the timed call
+    would have to write back)."""
+
+    def __init__(self, torch, a, b, c):
+        set_bytes = a.numel() * a.element_size() + b.numel() * b.element_size() + c.numel() * c.element_size()
+        n = max(2, -(-ROTATION_BYTES // max(set_bytes, 1)))
+        self.sets = [(a, b, c)] + [(a.clone(), b.clone(), torch.empty_like(c)) for _ in range(n - 1)]
+        self.next = 0
+
+    def time_ms(self, torch, stream, fn, reps):
+        """Mean time of `reps` calls fn(a, b, c), each on the set least recently
+        used (HIP events around each call); every set is used once, untimed,
+        before the first timed call."""
+        n = len(self.sets)
+        for _ in range(n):
+            fn(*self.sets[self.next])
+            self.next = (self.next + 1) % n
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+        for s0, s1 in ev:
+            s0.record(stream)
+            fn(*self.sets[self.next])
+            s1.record(stream)
+            self.next = (self.next + 1) % n
+        torch.cuda.synchronize()
+        return sum(x.elapsed_time(y) for x, y in ev) / reps
+
+
 def run_sweep(args, sg, torch, stream, dev):
     """The 125-shape sweep: the library's choice (SFC_TILE_AUTO, SFC_CA_AUTO),
-    timed cold (10 repetitions, 512 MiB flush between), and an autotune over
-    ca_layers in {1, 2, 4, 8, 16} with the model's block shape for each count."""
+    timed cold (10 repetitions in rotation over copies of the operands), and an
+    autotune over ca_layers in {1, 2, 4, 8, 16} with the model's block shape for
+    each count."""
     from paper_2601_16294_amd.inputs import draw, sweep_gemms
-    flush = torch.empty(512 * 1024 * 1024 // 4, dtype=torch.float32, device=dev)
     cus = torch.cuda.get_device_properties(dev).multi_processor_count
     occ = tuple(sg.sfc_gemm_plan(8192, 8192, 64, 1, t)["per_cu"] for t in ("128x128", "256x128", "128x256", "256x256"))
     mats = {}
@@ -116,15 +176,9 @@ def run_sweep(args, sg, torch, stream, dev):
             mats[seed] = sg.to_device_bf16(draw(rows, cols, dist, seed))
         return mats[seed]
 
-    def cold(a, b, c, layers, tile, reps):
-        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
-        for s0, s1 in ev:
-            flush.zero_()
-            s0.record(stream)
-            sg.sfc_gemm_ex(a, b, c, ca_layers=layers, tile=tile, stream=stream)
-            s1.record(stream)
-        torch.cuda.synchronize()
-        return sum(x.elapsed_time(y) for x, y in ev) / reps
+    def cold(sets, layers, tile, reps):
+        return sets.time_ms(torch, stream,
+                            lambda a, b, c: sg.sfc_gemm_ex(a, b, c, ca_layers=layers, tile=tile, stream=stream), reps)
 
     rows = []
     num = den = 0.0
@@ -133,14 +187,15 @@ def run_sweep(args, sg, torch, stream, dev):
         b = mat(g.K, g.N, g.dist_b, g.seed_b)
         c = torch.empty((g.M, g.N), dtype=torch.bfloat16, device=dev)
         choice = sg.sfc_gemm_model(g.M, g.N, g.K, out="bf16", num_cus=cus, occupancy=occ)
-        for _ in range(2):
-            sg.sfc_gemm_ex(a, b, c, ca_layers=0, tile="auto", stream=stream)
-        ms = cold(a, b, c, 0, "auto", args.reps)
+        warm_clock(torch, stream, lambda: sg.sfc_gemm_ex(a, b, c, ca_layers=0, tile="auto", stream=stream),
+                   args.warm_clock_ms / 4)
+        sets = ColdSets(torch, a, b, c)
+        ms = cold(sets, 0, "auto", args.reps)
         tuned = []
         for layers in (1, 2, 4, 8, 16):
             t = sg.sfc_gemm_model(g.M, g.N, g.K, out="bf16", ca_layers=layers, num_cus=cus, occupancy=occ)["tile"]
             sg.sfc_gemm_ex(a, b, c, ca_layers=layers, tile=t, stream=stream)
-            tuned.append((cold(a, b, c, layers, t, args.sweep_reps), t, layers))
+            tuned.append((cold(sets, layers, t, args.sweep_reps), t, layers))
         best = min(tuned)
         bound, roof = roofline_tflops(g.M, g.N, g.K, 2)
         tf = g.flops / (ms * 1e-3) / 1e12
@@ -152,14 +207,14 @@ def run_sweep(args, sg, torch, stream, dev):
         num += g.flops
         den += g.flops / tf
         log(f"[sweep] {g.M}x{g.N}x{g.K} {choice} {tf:.1f} TFLOP/s, best {rows[-1]['best']}")
-        del c
-    del flush, mats
+        del c, sets
+    del mats
     torch.cuda.empty_cache()
     best_num = sum(2.0 * r["M"] * r["N"] * r["K"] for r in rows)
     best_den = sum(2.0 * r["M"] * r["N"] * r["K"] / r["best"]["tflops"] for r in rows)
     ratio = [r["tflops"] / r["best"]["tflops"] for r in rows]
     return {"protocol": f"bf16 in, fp32 accumulate, bf16 out, U(-1,1); mean of {args.reps} cold reps "
-                        f"(512 MiB flush between) of the library's choice; autotune: ca_layers in "
+                        f"(in rotation over >= 1 GiB of operand copies) of the library's choice; autotune: ca_layers in "
                         f"{{1,2,4,8,16}} with the model's block shape, {args.sweep_reps} cold reps each",
             "whm_tflops": round(num / den, 2), "whm_tflops_autotuned": round(best_num / best_den, 2),
             "model_over_autotune_mean": round(sum(ratio) / len(ratio), 4),
@@ -212,18 +267,18 @@ def main():
     if args.only:
         # one workload's GEMMs (each called --steps times, in turn), for
         # profilers: --only-layers picks the layer count (default: the last of
-        # the workload's list), --only-tile the block shape, --cold flushes
-        # 512 MiB before every call, --fused sums the layer copies in the GEMM
+        # the workload's list), --only-tile the block shape, --cold takes the
+        # calls in rotation over copies of the operands (the cold protocol),
+        # --fused sums the layer copies in the GEMM
         ow = W[args.only]
         c_only = ow.ca_layers[-1] if args.only_layers is None else args.only_layers
-        flush = torch.empty(512 * 1024 * 1024 // 4, dtype=torch.float32, device=dev) if args.cold else None
         for og in ow.gemms:
             _, _, oA, oB, oC = prepare(og)
-            for _ in range(args.steps):
-                if flush is not None:
-                    flush.zero_()
-                run_once(oA, oB, oC, ow, c_only, tile=args.only_tile, fused=args.fused)
+            sets = ColdSets(torch, oA, oB, oC).sets if args.cold else [(oA, oB, oC)]
+            for i in range(args.steps):
+                run_once(*sets[i % len(sets)], ow, c_only, tile=args.only_tile, fused=args.fused)
             torch.cuda.synchronize()
+            del sets
             log(f"[bench] ran {args.only} {og.M}x{og.N}x{og.K} ca_layers={c_only} order={args.order} "
                 f"{'cold ' if args.cold else ''}{args.steps} times")
             del oA, oB, oC
@@ -242,6 +297,10 @@ def main():
     log(f"[bench] preparing {HEADLINE} {g.M}x{g.N}x{g.K}")
     A_host, B_host, dA, dB, C = prepare(g)
     plan = sg.sfc_gemm_plan(g.M, g.N, g.K, 1, w.tile)
+    # the GPU idled while the host drew the inputs: bring it to its loaded
+    # clock before the warm-up steps (reported in the line as clock_warmup)
+    head_ramp = warm_clock(torch, stream, lambda: run_once(dA, dB, C, w, 1), args.warm_clock_ms)
+    log(f"[bench] clock warm-up: ms per call {head_ramp[0]} (first batch) -> {head_ramp[1]} (last)")
     for _ in range(args.warmup):
         run_once(dA, dB, C, w, 1)
     torch.cuda.synchronize()
@@ -307,6 +366,7 @@ def main():
     a8 = sg.to_device_u8(draw_e4m3(g.M, g.K, ("normal", 0.0, 1.0), 2101))
     b8 = sg.to_device_u8(draw_e4m3(g.K, g.N, ("normal", 0.0, 1.0), 2102))
     c8 = torch.empty((g.M, g.N), dtype=torch.bfloat16, device=dev)
+    warm_clock(torch, stream, lambda: sg.sfc_gemm_f8_ex(a8, b8, c8, stream=stream), args.warm_clock_ms)
     for _ in range(args.warmup):
         sg.sfc_gemm_f8_ex(a8, b8, c8, stream=stream)
     torch.cuda.synchronize()
@@ -346,6 +406,8 @@ def main():
     from paper_2601_16294_amd.inputs import draw_fp8
     a5 = sg.to_device_u8(draw_fp8(g.M, g.K, ("normal", 0.0, 1.0), 2101, fmt="e5m2"))
     b5 = sg.to_device_u8(draw_fp8(g.K, g.N, ("normal", 0.0, 1.0), 2102, fmt="e5m2"))
+    warm_clock(torch, stream, lambda: sg.sfc_gemm_f8_ex(a5, b5, c8, stream=stream, a_format="e5m2", b_format="e5m2"),
+               args.warm_clock_ms / 2)
     for _ in range(args.warmup):
         sg.sfc_gemm_f8_ex(a5, b5, c8, stream=stream, a_format="e5m2", b_format="e5m2")
     torch.cuda.synchronize()
@@ -376,7 +438,6 @@ def main():
     # --------------------------------------------------------------- workloads
     table = None
     if not args.no_workloads:
-        flush = torch.empty(512 * 1024 * 1024 // 4, dtype=torch.float32, device=dev)
         table = {}
         whm_num = whm_den = 0.0
         for name, wl in W.items():
@@ -387,19 +448,18 @@ def main():
                 pm = sg.sfc_gemm_plan(x.M, x.N, x.K, 0, wl.tile)
                 entry["model_choice"].append({"tile": f"{pm['BM']}x{pm['BN']}", "ca_layers": pm["layers"]})
             ops = [prepare(gg)[2:] for gg in wl.gemms]
+            c_first = wl.ca_layers[0]
+            ramp = warm_clock(torch, stream,
+                              lambda: [run_once(a, b, cc, wl, c_first) for a, b, cc in ops], args.warm_clock_ms)
+            entry["clock_warmup"] = {"ms": args.warm_clock_ms, "first_batch_ms": ramp[0], "last_batch_ms": ramp[1]}
+            log(f"[bench] {name} clock warm-up: ms per call {ramp[0]} (first batch) -> {ramp[1]} (last)")
+
+            cold_sets = [ColdSets(torch, *op) for op in ops]
 
             def cold_ms(gi, c, reps, sched=None, tile=None, fused=False):
-                """Mean of `reps` cold calls (512 MiB flush before each, untimed)."""
-                a, b, cc = ops[gi]
-                ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-                      for _ in range(reps)]
-                for s, e in ev:
-                    flush.zero_()
-                    s.record(stream)
-                    run_once(a, b, cc, wl, c, sched, tile, fused)
-                    e.record(stream)
-                torch.cuda.synchronize()
-                return sum(s.elapsed_time(e) for s, e in ev) / reps
+                """Mean of `reps` cold calls (in rotation over copies of the operands)."""
+                return cold_sets[gi].time_ms(torch, stream,
+                                             lambda a, b, cc: run_once(a, b, cc, wl, c, sched, tile, fused), reps)
 
             def timed(c, sched=None, tile=None, fused=False):
                 cold_t = warm_t = 0.0
@@ -474,7 +534,7 @@ def main():
             if not args.no_autotune:
                 entry["model_vs_autotune"] = autotune()
                 log(f"[bench] {name} model vs autotune: {entry['model_vs_autotune']['model_over_best']}")
-            del ops
+            del ops, cold_sets
             best_c = max(per_c, key=lambda k: per_c[k]["tflops_cold"])
             best = per_c[best_c]
             # roofline of the workload: min(MFMA peak, OI x HBM) per GEMM with its
@@ -492,11 +552,11 @@ def main():
             whm_num += wl.flops
             whm_den += wl.flops / best["tflops_cold"]
             torch.cuda.empty_cache()
-        del flush
         whm = whm_num / whm_den
         best_shape = max(v["tflops"] for v in table.values())
         tuned = [v["model_vs_autotune"]["model_over_best"] for v in table.values() if "model_vs_autotune" in v]
-        table = {"protocol": f"mean of {args.reps} cold reps (512 MiB flush between), best ca_layers",
+        table = {"protocol": f"mean of {args.reps} cold reps (in rotation over >= 1 GiB of copies of A, B and C), "
+                             "best ca_layers",
                  "shapes": table, "whm_tflops": round(whm, 2),
                  "whm_over_best_shape": round(whm / best_shape, 4)}
         if tuned:
@@ -554,6 +614,8 @@ def main():
     line = {
         "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+        "clock_warmup": {"ms": args.warm_clock_ms, "first_batch_ms_per_step": head_ramp[0],
+                         "last_batch_ms_per_step": head_ramp[1]},
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "accumulate": "f32", "data": "synthetic",
         "config": {"workload": HEADLINE, "M": g.M, "N": g.N, "K": g.K, "out": g.out,

@@ -473,6 +473,8 @@ int gemm_noalloc_impl(int64_t M, int64_t N, int64_t K, const void* A, int64_t ld
   Plan pl;
   rc = make_plan(*st, M, N, K, A, lda, B, ldb, ob, ca_layers, tile, &pl);
   if (rc != SFC_OK) return rc;
+  if (pl.ce > 1 && (size_t)pl.ce * (size_t)M * (size_t)N * 4u > kNoAllocWsBytes)
+    return set_error(SFC_ERR_WORKSPACE, "sfc_gemm_noalloc_ex: the planned layer copies exceed its workspace");
   Split sp;
   if (tile == SFC_TILE_AUTO) {
     rc = plan_tail_split(*st, pl, M, N, K, A, lda, B, ldb, ob, &sp);
