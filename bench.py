@@ -420,8 +420,30 @@ def main():
     f5_ms = sum(x.elapsed_time(y) for x, y in ev5) / args.steps
     fp8["e5m2"] = {"call": "sfc_gemm_f8_fmt_ex, E5M2 A and B ~ N(0,1), bf16 out", "ms": round(f5_ms, 4),
                    "tflops": round(g.flops / (f5_ms * 1e-3) / 1e12, 1)}
+    # the fp8 block shapes on a ragged grid: the model's choice (128x256 here)
+    # against 256x256 blocks, warm, E4M3 in and bf16 out
+    rM, rN, rK = 3000, 7008, 2048
+    ra8 = sg.to_device_u8(draw_e4m3(rM, rK, ("normal", 0.0, 1.0), 2103))
+    rb8 = sg.to_device_u8(draw_e4m3(rK, rN, ("normal", 0.0, 1.0), 2104))
+    rc8 = torch.empty((rM, rN), dtype=torch.bfloat16, device=dev)
+    shapes8 = {}
+    for t in ("auto", "256x256"):
+        fn8 = lambda: sg.sfc_gemm_f8_ex(ra8, rb8, rc8, tile=t, stream=stream)
+        warm_clock(torch, stream, fn8, args.warm_clock_ms / 4)
+        s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s0.record(stream)
+        for _ in range(20):
+            fn8()
+        s1.record(stream)
+        torch.cuda.synchronize()
+        ms8 = s0.elapsed_time(s1) / 20
+        key = "model_choice" if t == "auto" else t
+        shapes8[key] = {"ms": round(ms8, 4), "tflops": round(2.0 * rM * rN * rK / (ms8 * 1e-3) / 1e12, 1)}
+    pl8 = sg.sfc_gemm_f8_plan(rM, rN, rK, 1, "auto")
+    shapes8["model_choice"]["tile"] = f"{pl8['BM']}x{pl8['BN']}"
+    fp8["ragged3000x7008x2048"] = shapes8
     log(f"[bench] fp8 {fp8}")
-    del a8, b8, c8, a5, b5
+    del a8, b8, c8, a5, b5, ra8, rb8, rc8
     torch.cuda.empty_cache()
 
     # ---------------------------------------------- sustained MFMA throughput

@@ -217,12 +217,13 @@ int sfc_gemm_noalloc_ex(int64_t M, int64_t N, int64_t K,
  * K-layer scheme, with K blocks 128 deep: ca_layers = c uses min(c,
  * ceil(K/128)) layers, whose workspace sfc_gemm_ws_size(M, N, K, c) bounds.
  * Restrictions (else SFC_ERR_UNSUPPORTED, nothing enqueued): A and B 16-byte
- * aligned, lda, ldb, K and N multiples of 16; tile SFC_TILE_AUTO or
- * SFC_TILE_256x256 (256x256 blocks).  ca_layers = SFC_CA_AUTO picks the layer
- * count with the model of sfc_gemm_model for 256x256 blocks, evaluated on the
- * bf16 problem with the same number of K blocks (K' = 64*ceil(K/128)): a
- * 128-deep fp8 block moves the bytes of a 64-deep bf16 block and takes the same
- * MFMA time.  Other arguments and errors as for sfc_gemm_ex.
+ * aligned, lda, ldb, K and N multiples of 16; tile SFC_TILE_AUTO,
+ * SFC_TILE_256x256 or SFC_TILE_128x256.  SFC_TILE_AUTO and SFC_CA_AUTO pick the
+ * free knobs with the model of sfc_gemm_model over those two block shapes,
+ * evaluated on the bf16 problem with the same number of K blocks (K' =
+ * 64*ceil(K/128)): a 128-deep fp8 block moves the bytes of a 64-deep bf16
+ * block and takes the same MFMA time (ties go to 256x256).  Other arguments and
+ * errors as for sfc_gemm_ex.
  */
 int sfc_gemm_f8_ex(int64_t M, int64_t N, int64_t K,
                    const void *A, int64_t lda,
@@ -262,6 +263,14 @@ int sfc_gemm_f8_fmt_ex(int64_t M, int64_t N, int64_t K,
  * Needs a device (it queries the CU count and kernel occupancy).
  */
 int sfc_gemm_plan(int64_t M, int64_t N, int64_t K, int ca_layers, int tile, int64_t plan[7]);
+
+/*
+ * sfc_gemm_f8_plan -- what sfc_gemm_f8_ex (and sfc_gemm_f8_fmt_ex) would
+ * launch, without launching (fp32 output); plan[] as for sfc_gemm_plan.  tile
+ * is SFC_TILE_AUTO, SFC_TILE_128x256 or SFC_TILE_256x256, else
+ * SFC_ERR_INVALID_ARG.  Needs a device.
+ */
+int sfc_gemm_f8_plan(int64_t M, int64_t N, int64_t K, int ca_layers, int tile, int64_t plan[7]);
 
 /*
  * sfc_gemm_model -- the analytical model behind SFC_TILE_AUTO and SFC_CA_AUTO,

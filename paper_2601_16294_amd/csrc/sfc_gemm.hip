@@ -369,7 +369,7 @@ __device__ __forceinline__ void ring_lanes(const GemmParams& p, int64_t m0, int6
 // Turn the A lanes whose load starts at a K index >= kin (within the block)
 // into out-of-range lanes, for the loads of a block that runs past K.
 template <int BM, int BN, int NW, int F8>
-__device__ __forceinline__ void mask_a_lanes(RingLanes<BM, BN, NW, F8>& L, int wave, int lane, int64_t kin) {
+__device__ __forceinline__ void mask_a_lanes(RingLanes<BM, BN, NW, F8>& L, int wave, int lane, int kin) {
   using R = Ring<BM, BN, NW, F8>;
 #pragma unroll
   for (int j = 0; j < R::APB; ++j)
@@ -378,7 +378,7 @@ __device__ __forceinline__ void mask_a_lanes(RingLanes<BM, BN, NW, F8>& L, int w
 
 // The same without a branch: masks only when `on` (wave-uniform).
 template <int BM, int BN, int NW, int F8>
-__device__ __forceinline__ void mask_a_lanes_if(RingLanes<BM, BN, NW, F8>& L, int wave, int lane, int64_t kin, bool on) {
+__device__ __forceinline__ void mask_a_lanes_if(RingLanes<BM, BN, NW, F8>& L, int wave, int lane, int kin, bool on) {
   using R = Ring<BM, BN, NW, F8>;
 #pragma unroll
   for (int j = 0; j < R::APB; ++j)
@@ -517,7 +517,9 @@ __device__ __forceinline__ void dma_all(const SlotDma& d, const RingLanes<BM, BN
 //           (the order the next step's MFMAs consume them), spread evenly;
 //   loads:  each load pair becomes three operations (set M0, load, load) in
 //           consecutive groups from evenly spaced starting groups, so that the
-//           MFMA between M0 and the first load covers the wait M0 needs.
+//           MFMA between M0 and the first load covers the wait M0 needs; a
+//           step with fewer free groups than that needs (fp8 128x256: 8 MFMAs
+//           of 64 cycles) issues each pair whole in one group, evenly spaced.
 template <int BM, int BN, int NW, int F8, int OP>
 struct StepPlan {
   using T = Tile<BM, BN, NW, F8>;
@@ -528,15 +530,18 @@ struct StepPlan {
   static constexpr int NP0 = OP == 1 ? Ring<BM, BN, NW, F8>::APB / 2 : Ring<BM, BN, NW, F8>::BPW / 2;   // pairs from d0
   static constexpr int NP1 = OP == 1 ? 0 : Ring<BM, BN, NW, F8>::BPW / 2;                      // pairs from d1
   static constexpr int NP = NP0 + NP1;
-  static constexpr int ND = 3 * NP;
   // the B step opens with G0 groups of MFMAs alone and then waits at the
   // block's barrier: those MFMAs need nothing the barrier publishes, and they
   // keep the matrix core busy while the waves meet and while the A step's last
   // fragment reads (which the barrier waits for) complete; steps of 32 or more
   // MFMAs open with 4 (measured best of 2, 4, 6, 8), shorter ones with 2
   static constexpr int G0 = OP == 2 ? (T::FM * T::FN >= 32 ? 4 : 2) : 0;
+  // whole pairs: one operation per pair (M0, a wait state and both loads)
+  static constexpr bool WHOLE = 3 * NP > G - G0;
+  static constexpr int ND = WHOLE ? NP : 3 * NP;
   static constexpr int read_group(int r) { return G0 + (r * (G - G0)) / NR; }
   static constexpr int dma_group(int o) {
+    if (WHOLE) return G0 + ((2 * o + 1) * (G - G0)) / (2 * NP);
     int g = G0 - 1;
     for (int i = 0; i <= o; ++i) {
       const int start = G0 + ((2 * (i / 3) + 1) * (G - G0)) / (2 * NP) - 1 + i % 3;
@@ -569,10 +574,18 @@ struct StepPlan {
     }
     return (s * G) / ns;
   }
-  // bf16: at most one read beside each 16-cycle MFMA; fp8: two beside each
-  // 64-cycle MFMA
-  static_assert(NR <= (F8 ? 2 : 1) * (G - G0), "reads per group");
+  // the first load of A pair q (lanes 2q, 2q+1) comes after the K-mask
+  // selects of those lanes, which run on groups 2q and 2q+1
+  static constexpr bool a_loads_after_masks() {
+    for (int q = 0; q < NP; ++q)
+      if (dma_group(WHOLE ? q : 3 * q + 1) <= 2 * q + 1) return false;
+    return true;
+  }
+  // bf16: at most one read beside each 16-cycle MFMA; fp8: up to three beside
+  // each 64-cycle MFMA
+  static_assert(NR <= (F8 ? 3 : 1) * (G - G0), "reads per group");
   static_assert(ND == 0 || dma_group(ND - 1) < G, "loads fit in the step");
+  static_assert(OP != 1 || a_loads_after_masks(), "A loads after their K-mask selects");
 };
 
 // Per-step state of the split B reads: address and low half of each fragment.
@@ -623,23 +636,29 @@ __device__ __forceinline__ void group_reads(uint32_t a_base, uint32_t b_slot, co
 }
 
 // Load operation o of a step: o = 3q + k for load pair q (k 0: set M0, k 1
-// and 2: the pair's loads).
+// and 2: the pair's loads), or load pair o whole.
 template <int BM, int BN, int NW, int F8, int OP, int o>
 __device__ __forceinline__ void step_dma(const SlotDma& d0, const SlotDma& d1, const RingLanes<BM, BN, NW, F8>& L) {
   using P = StepPlan<BM, BN, NW, F8, OP>;
-  constexpr int q = o / 3, k = o % 3;
-  constexpr bool first = q < P::NP0;
-  constexpr int qq = first ? q : q - P::NP0;
-  const SlotDma& d = first ? d0 : d1;
-  constexpr int j = 2 * qq + (k == 2 ? 1 : 0);
-  if constexpr (k == 0) {
-    const uint32_t m0v = OP == 1 ? d.m0 + (uint32_t)((j >> 2) * 4096) : d.m0;
-    asm volatile("s_mov_b32 m0, %0" :: "s"(m0v) : "memory");
+  if constexpr (P::WHOLE) {
+    // operation o is load pair o, whole
+    if constexpr (o < P::NP0) dma_pair<BM, BN, NW, F8, OP, o>(d0, L);
+    else dma_pair<BM, BN, NW, F8, OP, o - P::NP0>(d1, L);
   } else {
-    constexpr int off = OP == 1 ? (j & 3) * 1024 : j * 1024;
-    static_assert(off <= 4095, "instruction offset range");
-    const int v = OP == 1 ? L.a_voff[j] : L.b_voff[j];
-    asm volatile("buffer_load_dwordx4 %0, %1, 0 offen offset:%2 lds" :: "v"(v), "s"(d.rsrc), "n"(off) : "memory");
+    constexpr int q = o / 3, k = o % 3;
+    constexpr bool first = q < P::NP0;
+    constexpr int qq = first ? q : q - P::NP0;
+    const SlotDma& d = first ? d0 : d1;
+    constexpr int j = 2 * qq + (k == 2 ? 1 : 0);
+    if constexpr (k == 0) {
+      const uint32_t m0v = OP == 1 ? d.m0 + (uint32_t)((j >> 2) * 4096) : d.m0;
+      asm volatile("s_mov_b32 m0, %0" :: "s"(m0v) : "memory");
+    } else {
+      constexpr int off = OP == 1 ? (j & 3) * 1024 : j * 1024;
+      static_assert(off <= 4095, "instruction offset range");
+      const int v = OP == 1 ? L.a_voff[j] : L.b_voff[j];
+      asm volatile("buffer_load_dwordx4 %0, %1, 0 offen offset:%2 lds" :: "v"(v), "s"(d.rsrc), "n"(off) : "memory");
+    }
   }
 }
 
@@ -749,7 +768,7 @@ __device__ __forceinline__ uint32_t b_stage_limit(const RingAddr& ra, int x) {
 // its lanes past K masked (selects on the first groups of the step that issues
 // those loads, or in the prologue when nb <= D).
 template <int BM, int BN, int NW, int F8, int D>
-__device__ __forceinline__ void main_loop_ring(const RingAddr& ra, int nb, int64_t kin_last,
+__device__ __forceinline__ void main_loop_ring(const RingAddr& ra, int nb, int kin_last,
                                                const ReadOffsets<BM, BN, NW, F8>& o, RingLanes<BM, BN, NW, F8>& L, int lane,
                                                Acc<BM, BN, NW, F8>& acc) {
   using R = Ring<BM, BN, NW, F8, D>;
@@ -1470,8 +1489,12 @@ __global__ __launch_bounds__(NW * 64, 1) void sfc_gemm_kernel(GemmParams p) {
         }
         ra.lds0 = lds_addr(smem);
         ra.wave = wave;
-        main_loop_ring<BM, BN, NW, F8, D>(ra, kt1 - kt0, p.K - (int64_t)(kt1 - 1) * block_k<F8>(), ro, L, lane_t,
-                                       acc);
+        // K elements of the task's last block that lie before K (a full
+        // block unless the block runs past K), in 32 bits: the per-lane K-mask
+        // compares then stay single registers
+        const int64_t kin64 = p.K - (int64_t)(kt1 - 1) * block_k<F8>();
+        const int kin_last = kin64 < block_k<F8>() ? (int)kin64 : block_k<F8>();
+        main_loop_ring<BM, BN, NW, F8, D>(ra, kt1 - kt0, kin_last, ro, L, lane_t, acc);
       } else if constexpr (!F8) {
         main_loop_staged<BM, BN, NW, F8>(p, smem, m0, n0, kt0, kt1, tid, acc);
       }
@@ -1513,10 +1536,13 @@ static const void* kernel_ptr() {
 }
 
 // fp8 operands (f8 = 1 + a + 2b, a and b the formats of A and B: 0 OCP E4M3,
-// 1 OCP E5M2): 256x256 blocks, fast path only.
+// 1 OCP E5M2): 256x256 or 128x256 blocks, fast path only.
 static const void* select_kernel_f8(int tile, bool ob, int f8) {
-  if (tile != kT256x256) return nullptr;
-#define SFC_K8(F_) return ob ? kernel_ptr<256, 256, 4, F_, true, true>() : kernel_ptr<256, 256, 4, F_, false, true>()
+  if (tile != kT256x256 && tile != kT128x256) return nullptr;
+  const bool wide = tile == kT256x256;
+#define SFC_K8(F_)                                                                                        \
+  return wide ? (ob ? kernel_ptr<256, 256, 4, F_, true, true>() : kernel_ptr<256, 256, 4, F_, false, true>()) \
+              : (ob ? kernel_ptr<128, 256, 4, F_, true, true>() : kernel_ptr<128, 256, 4, F_, false, true>())
   switch (f8) {
     case 1: SFC_K8(1);
     case 2: SFC_K8(2);

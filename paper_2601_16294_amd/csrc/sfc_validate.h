@@ -142,8 +142,8 @@ inline Checked check_gemm_f8_args(int64_t M, int64_t N, int64_t K, const void* A
   Checked c = check_gemm_args(M, N, K, A, lda, B, ldb, C, ldc, out_type, ca_layers, tile, order, sched, ws,
                               ws_bytes);
   if (c.code != SFC_OK || M == 0 || N == 0) return c;
-  if (tile != SFC_TILE_AUTO && tile != SFC_TILE_256x256)
-    return fail(SFC_ERR_UNSUPPORTED, "fp8 operands run on 256x256 blocks");
+  if (tile != SFC_TILE_AUTO && tile != SFC_TILE_256x256 && tile != SFC_TILE_128x256)
+    return fail(SFC_ERR_UNSUPPORTED, "fp8 operands run on 256x256 or 128x256 blocks");
   if (K > 0 && !f8_loads_ok(A, lda, B, ldb, K, N))
     return fail(SFC_ERR_UNSUPPORTED,
                 "fp8 operands need 16-byte aligned A and B and lda, ldb, K, N multiples of 16");

@@ -201,25 +201,38 @@ int make_plan(DeviceState& st, int64_t M, int64_t N, int64_t K, const void* A, i
               const void* B, int64_t ldb, bool ob, int ca_layers, int tile_api, Plan* pl, int f8 = 0) {
   int rc = SFC_OK;
   if (f8) {
-    // fp8 operands (checked by check_gemm_f8_args): 256x256 blocks, 128-deep K
-    // blocks.  A 128-deep fp8 block moves the bytes of a 64-deep bf16 block and
-    // takes the same MFMA time, so SFC_CA_AUTO asks the model about the bf16
-    // problem with the same number of blocks.
+    // fp8 operands (checked by check_gemm_f8_args): 256x256 or 128x256 blocks,
+    // 128-deep K blocks.  A 128-deep fp8 block moves the bytes of a 64-deep
+    // bf16 block and takes the same MFMA time, so the free knobs are chosen by
+    // the model for the bf16 problem with the same number of blocks, over the
+    // two fp8 block shapes (256x256 first: it keeps a tie).
     pl->vec = true;
-    pl->tile = sfc::kT256x256;
-    int layers = ca_layers;
-    if (ca_layers == SFC_CA_AUTO) {
-      int occ[sfc::kNumTiles];
-      for (int t = 0; t < sfc::kNumTiles; ++t) occ[t] = 1;
-      rc = get_occupancy(st, sfc::kT256x256, ob, true, &occ[sfc::kT256x256], f8);
+    int occ[sfc::kNumTiles];
+    for (int t = 0; t < sfc::kNumTiles; ++t) occ[t] = 1;
+    static const int kF8Tiles[2] = {sfc::kT256x256, sfc::kT128x256};
+    for (int t : kF8Tiles) {
+      rc = get_occupancy(st, t, ob, true, &occ[t], f8);
       if (rc != SFC_OK) return rc;
-      const int64_t k_equiv = (K > 0 ? sfc::ceil_div(K, 128) : 0) * sfc::kBK;
-      layers = sfc::model_choose(M, N, k_equiv, ob ? 2 : 4, st.num_cus, occ, sfc::kT256x256, SFC_CA_AUTO).layers;
     }
+    int tile = tile_api == SFC_TILE_AUTO ? -1 : tile_from_api(tile_api);
+    int layers = ca_layers;
+    if (tile < 0 || ca_layers == SFC_CA_AUTO) {
+      const int64_t k_equiv = (K > 0 ? sfc::ceil_div(K, 128) : 0) * sfc::kBK;
+      sfc::ModelChoice best{-1, 1, 0.0};
+      for (int t : kF8Tiles) {
+        if (tile >= 0 && t != tile) continue;
+        const sfc::ModelChoice ch = sfc::model_choose(M, N, k_equiv, ob ? 2 : 4, st.num_cus, occ, t, ca_layers);
+        if (best.tile < 0 || ch.clk < best.clk) best = ch;
+      }
+      tile = best.tile;
+      layers = best.layers;
+    }
+    pl->tile = tile;
     pl->ce = sfc::effective_layers(K, layers, 128);
-    pl->bm = pl->bn = 256;
-    pl->gm = (int)sfc::ceil_div(M, 256);
-    pl->gn = (int)sfc::ceil_div(N, 256);
+    pl->bm = sfc::tile_bm(tile);
+    pl->bn = sfc::tile_bn(tile);
+    pl->gm = (int)sfc::ceil_div(M, pl->bm);
+    pl->gn = (int)sfc::ceil_div(N, pl->bn);
     pl->nk = (int)(K > 0 ? sfc::ceil_div(K, 128) : 0);
     rc = get_occupancy(st, pl->tile, ob && pl->ce == 1, true, &pl->occ, f8);
     if (rc != SFC_OK) return rc;
@@ -641,6 +654,23 @@ int sfc_gemm_plan(int64_t M, int64_t N, int64_t K, int ca_layers, int tile, int6
   // aligned dummy pointers: the plan of the vector-load path
   rc = make_plan(*st, M, N, K, reinterpret_cast<const void*>(256), (K + 7) / 8 * 8,
                  reinterpret_cast<const void*>(256), (N + 7) / 8 * 8, false, ca_layers, tile, &pl);
+  if (rc != SFC_OK) return rc;
+  plan[0] = pl.bm; plan[1] = pl.bn; plan[2] = pl.gm; plan[3] = pl.gn;
+  plan[4] = pl.ce; plan[5] = pl.grid; plan[6] = pl.occ;
+  return SFC_OK;
+}
+
+int sfc_gemm_f8_plan(int64_t M, int64_t N, int64_t K, int ca_layers, int tile, int64_t plan[7]) {
+  if (!plan) return set_error(SFC_ERR_INVALID_ARG, "plan is NULL");
+  if (M <= 0 || N <= 0 || K < 0 || ca_layers < 0 || ca_layers > sfc::kMaxLayers ||
+      (tile != SFC_TILE_AUTO && tile != SFC_TILE_128x256 && tile != SFC_TILE_256x256))
+    return set_error(SFC_ERR_INVALID_ARG, "invalid plan arguments");
+  std::lock_guard<std::mutex> lock(g_mu);
+  DeviceState* st = nullptr;
+  int rc = device_state(&st);
+  if (rc != SFC_OK) return rc;
+  Plan pl;
+  rc = make_plan(*st, M, N, K, nullptr, 0, nullptr, 0, false, ca_layers, tile, &pl, 1);
   if (rc != SFC_OK) return rc;
   plan[0] = pl.bm; plan[1] = pl.bn; plan[2] = pl.gm; plan[3] = pl.gn;
   plan[4] = pl.ce; plan[5] = pl.grid; plan[6] = pl.occ;

@@ -34,7 +34,7 @@ SCHEDS = {"interleaved": 0, "block": 1, "interleaved_plain": 2}
 
 # Every symbol include/sfcgemm.h declares.
 EXPORTS = ["sfc_tile_order", "sfc_tile_order_ex", "sfc_gemm", "sfc_gemm_bf16out", "sfc_gemm_ws_size",
-           "sfc_gemm_ex", "sfc_gemm_fused_ex", "sfc_gemm_noalloc_ex", "sfc_gemm_f8_ex", "sfc_gemm_f8_fmt_ex", "sfc_gemm_plan", "sfc_gemm_model", "sfc_probe_mfma", "sfc_strerror",
+           "sfc_gemm_ex", "sfc_gemm_fused_ex", "sfc_gemm_noalloc_ex", "sfc_gemm_f8_ex", "sfc_gemm_f8_fmt_ex", "sfc_gemm_plan", "sfc_gemm_f8_plan", "sfc_gemm_model", "sfc_probe_mfma", "sfc_strerror",
            "sfc_last_error", "sfc_version"]
 
 
@@ -73,6 +73,8 @@ def _load() -> ctypes.CDLL:
     lib.sfc_gemm_ws_size.restype = sz
     lib.sfc_gemm_plan.argtypes = [i64, i64, i64, i32, i32, ctypes.POINTER(ctypes.c_int64)]
     lib.sfc_gemm_plan.restype = i32
+    lib.sfc_gemm_f8_plan.argtypes = [i64, i64, i64, i32, i32, ctypes.POINTER(ctypes.c_int64)]
+    lib.sfc_gemm_f8_plan.restype = i32
     lib.sfc_gemm_model.argtypes = [i64, i64, i64, i32, i32, i32, i32, ctypes.POINTER(ctypes.c_int32),
                                    ctypes.POINTER(ctypes.c_int64)]
     lib.sfc_gemm_model.restype = i32
@@ -117,6 +119,14 @@ def sfc_gemm_ws_size(M: int, N: int, K: int, ca_layers: int) -> int:
 def sfc_gemm_plan(M: int, N: int, K: int, ca_layers: int = 1, tile: str = "auto") -> dict:
     plan = (ctypes.c_int64 * 7)()
     _check(lib.sfc_gemm_plan(M, N, K, ca_layers, TILES[tile], plan), "sfc_gemm_plan")
+    keys = ["BM", "BN", "gm", "gn", "layers", "workgroups", "per_cu"]
+    return dict(zip(keys, [int(v) for v in plan]))
+
+
+def sfc_gemm_f8_plan(M: int, N: int, K: int, ca_layers: int = 1, tile: str = "auto") -> dict:
+    """What sfc_gemm_f8_ex would launch (fp32 output), as sfc_gemm_plan."""
+    plan = (ctypes.c_int64 * 7)()
+    _check(lib.sfc_gemm_f8_plan(M, N, K, ca_layers, TILES[tile], plan), "sfc_gemm_f8_plan")
     keys = ["BM", "BN", "gm", "gn", "layers", "workgroups", "per_cu"]
     return dict(zip(keys, [int(v) for v in plan]))
 

@@ -116,6 +116,10 @@ def test_plan_validation(sg):
     plan = (ctypes.c_int64 * 7)()
     assert sg.lib.sfc_gemm_plan(0, 4, 4, 1, 0, plan) == -1
     assert sg.lib.sfc_gemm_plan(4, 4, 4, 1, 0, None) == -1
+    assert sg.lib.sfc_gemm_f8_plan(0, 4, 4, 1, 0, plan) == -1
+    assert sg.lib.sfc_gemm_f8_plan(4, 4, 4, 1, 0, None) == -1
+    for tile in (1, 2, 5):   # fp8 runs 128x256 and 256x256 blocks only
+        assert sg.lib.sfc_gemm_f8_plan(64, 64, 64, 1, tile, plan) == -1
 
 
 def test_probe_validation(sg):
@@ -142,7 +146,7 @@ def call_f8(sg, **kw):
     (dict(N=40, ldb=64, ldc=64), -2),         # N not a multiple of 16
     (dict(lda=72), -2), (dict(ldb=72), -2),   # leading dimensions not multiples of 16
     (dict(A=4096 + 8), -2), (dict(B=8192 + 8), -2),   # rows not 16-byte aligned
-    (dict(tile=1), -2), (dict(tile=2), -2), (dict(tile=3), -2),
+    (dict(tile=1), -2), (dict(tile=2), -2),    # no 128x128 or 256x128 fp8 kernel
     (dict(lda=1 << 21), -2), (dict(ldb=1 << 23), -2),   # past the 32-bit per-lane offsets; no element path
     (dict(c=2, K=256, lda=256, ws=1 << 20, wsb=2 * 64 * 64 * 4 - 1), -3),
 ])

@@ -1,7 +1,9 @@
 """Parity of the fp8 (OCP E4M3) GEMM path (sfc_gemm_f8_ex, through the C ABI)
 with the fp64 oracle over the decoded operands: ragged M, K tails inside a
-128-deep block, several layer counts, both output types, exact integer
-inputs, the bf16 output as RNE of the fp32 output, and the argument checks."""
+128-deep block, several layer counts, both output types, both block shapes
+(256x256 and 128x256, which give the same bits), exact integer inputs, the
+bf16 output as RNE of the fp32 output, the model's choice of block shape, and
+the argument checks."""
 import numpy as np
 import pytest
 import torch
@@ -26,12 +28,12 @@ def ref(A8, B8, M, N, K):
     return ogemm.gemm_ref_rows(A, B, N, K, K, N, M=M)
 
 
-def run8(A8, B8, M, N, K, out="f32", c=1, ldc=None):
+def run8(A8, B8, M, N, K, out="f32", c=1, ldc=None, tile="auto"):
     ldc = N if ldc is None else ldc
     dtype = torch.float32 if out == "f32" else torch.bfloat16
     Cfull = torch.full((M, ldc), float("nan"), dtype=dtype, device="cuda")
     dA, dB = up8(A8), up8(B8)
-    sg().sfc_gemm_f8_ex(dA[:M, :K], dB[:K, :N], Cfull[:, :N], ca_layers=c)
+    sg().sfc_gemm_f8_ex(dA[:M, :K], dB[:K, :N], Cfull[:, :N], ca_layers=c, tile=tile)
     torch.cuda.synchronize()
     return Cfull
 
@@ -51,6 +53,50 @@ def test_ragged_shapes(M, N, K, out):
         ocheck.assert_gemm_close(C, Cr, R, f"fp8 {M}x{N}x{K} {out} c={c}")
 
 
+@pytest.mark.parametrize("M,N,K", SHAPES)
+@pytest.mark.parametrize("out", ["f32", "bf16"])
+def test_ragged_shapes_128x256(M, N, K, out):
+    """The 128x256 fp8 kernel (4 waves of 128x64, 8 MFMAs per 64-deep step)."""
+    A = draw_e4m3(M, K, ("normal", 0.0, 1.0), 5 * M + K)
+    B = draw_e4m3(K, N, ("normal", 0.0, 1.0), 5 * N + K + 1)
+    Cr, R = ref(A, B, M, N, K)
+    for c in (1, 3):
+        C = to_host(run8(A, B, M, N, K, out, c, tile="128x256"))
+        ocheck.assert_gemm_close(C, Cr, R, f"fp8 128x256 {M}x{N}x{K} {out} c={c}")
+
+
+def test_block_shapes_give_the_same_bits():
+    """Each output element takes the same MFMA products in the same K order on
+    either block shape, so 128x256 and 256x256 blocks give identical bits (one
+    layer), here on a grid with ragged edges in both directions."""
+    M, N, K = 700, 912, 1296
+    A = draw_e4m3(M, K, ("normal", 0.0, 1.0), 8801)
+    B = draw_e4m3(K, N, ("normal", 0.0, 1.0), 8802)
+    for out in ("f32", "bf16"):
+        Cw = run8(A, B, M, N, K, out, tile="256x256")
+        Cn = run8(A, B, M, N, K, out, tile="128x256")
+        assert np.array_equal(raw_bits(Cw), raw_bits(Cn)), out
+
+
+@pytest.mark.parametrize("M,N,K,c", [(8192, 640, 4096, 1), (1536, 2048, 1024, 1), (1024, 1024, 16384, 0),
+                                     (300, 272, 1040, 0)])
+def test_auto_block_shape_follows_the_model(M, N, K, c):
+    """SFC_TILE_AUTO on fp8 operands: the block shape and layer count of the
+    oracle's model over the two fp8 block shapes for the equivalent bf16
+    problem (K' = 64*ceil(K/128)), at the fp8 kernels' occupancy."""
+    from oracle import model as omodel
+    plan = sg().sfc_gemm_f8_plan(M, N, K, c, "auto")
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    occ = {(128, 128): 1, (256, 128): 1,
+           (128, 256): sg().sfc_gemm_f8_plan(8192, 8192, 128, 1, "128x256")["per_cu"],
+           (256, 256): sg().sfc_gemm_f8_plan(8192, 8192, 128, 1, "256x256")["per_cu"]}
+    k_eq = 64 * -(-K // 128)
+    picks = [omodel.choose(M, N, k_eq, 4, cus, occ, shape=s, layers=c) for s in ((256, 256), (128, 256))]
+    best = picks[1] if picks[1][2] < picks[0][2] else picks[0]
+    assert (plan["BM"], plan["BN"]) == best[0]
+    assert plan["layers"] == min(best[1], -(-K // 128))
+
+
 @pytest.mark.parametrize("c", [1, 2, 5])
 def test_integer_inputs_exact(c):
     M, N, K = 300, 272, 1040
@@ -58,8 +104,9 @@ def test_integer_inputs_exact(c):
     B = draw_e4m3(K, N, ("int", -4, 4), 32)
     Ai = of8.e4m3_to_f64(A).astype(np.int64)
     Bi = of8.e4m3_to_f64(B).astype(np.int64)
-    C = to_host(run8(A, B, M, N, K, "f32", c))
-    assert np.array_equal(C, (Ai @ Bi).astype(np.float64))
+    for tile in ("256x256", "128x256"):
+        C = to_host(run8(A, B, M, N, K, "f32", c, tile=tile))
+        assert np.array_equal(C, (Ai @ Bi).astype(np.float64)), tile
 
 
 def test_bf16_output_is_rne_of_f32_output_and_padding_untouched():
@@ -152,10 +199,11 @@ def test_formats_against_oracle(fa, fb, M, N, K, c, out):
     B = draw_fp8(K, N, ("normal", 0.0, 1.0), seed + 1, fmt=fb)
     Cr, R = ref_fmt(A, B, M, N, K, fa, fb)
     dtype = torch.float32 if out == "f32" else torch.bfloat16
-    C = torch.full((M, N), float("nan"), dtype=dtype, device="cuda")
-    sg().sfc_gemm_f8_ex(up8(A), up8(B), C, ca_layers=c, a_format=fa, b_format=fb)
-    torch.cuda.synchronize()
-    ocheck.assert_gemm_close(to_host(C), Cr, R, f"{fa} x {fb} {M}x{N}x{K} c={c} {out}")
+    for tile in ("256x256", "128x256"):
+        C = torch.full((M, N), float("nan"), dtype=dtype, device="cuda")
+        sg().sfc_gemm_f8_ex(up8(A), up8(B), C, ca_layers=c, tile=tile, a_format=fa, b_format=fb)
+        torch.cuda.synchronize()
+        ocheck.assert_gemm_close(to_host(C), Cr, R, f"{fa} x {fb} {M}x{N}x{K} c={c} {out} {tile}")
 
 
 @pytest.mark.parametrize("fa,fb", FMT_PAIRS)
@@ -166,10 +214,11 @@ def test_formats_integers_exact(fa, fb):
     B = draw_fp8(K, N, ("int", -8, 8), 9802, fmt=fb)
     Cr, _ = ref_fmt(A, B, M, N, K, fa, fb)
     for c in (1, 4):
-        C = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
-        sg().sfc_gemm_f8_ex(up8(A), up8(B), C, ca_layers=c, a_format=fa, b_format=fb)
-        torch.cuda.synchronize()
-        assert np.array_equal(to_host(C), Cr), f"{fa} x {fb} c={c}"
+        for tile in ("256x256", "128x256"):
+            C = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
+            sg().sfc_gemm_f8_ex(up8(A), up8(B), C, ca_layers=c, tile=tile, a_format=fa, b_format=fb)
+            torch.cuda.synchronize()
+            assert np.array_equal(to_host(C), Cr), f"{fa} x {fb} c={c} {tile}"
 
 
 def test_format_codes_select_the_format():

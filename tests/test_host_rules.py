@@ -101,7 +101,7 @@ def test_deep_ring_rule(deep_harness):
         (1, 1, 0, 1320, 256): 0,
         (0, 1, 0, 16, 256): 0,      # other block shapes fill the LDS already
         (1, 0, 0, 16, 256): 0,      # element-load path
-        (1, 1, 1, 16, 256): 0,      # fp8 operands run 256x256 blocks
+        (1, 1, 1, 16, 256): 0,      # fp8 operands have no 128x128 kernel
         (1, 1, 0, 0, 256): 0,
     }
     args = [str(v) for c in cases for v in c]
