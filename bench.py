@@ -76,7 +76,8 @@ def parse():
     ap.add_argument("--warm-clock-ms", type=float, default=200.0,
                     help="back-to-back calls of a workload before it is timed (sweep shapes: a quarter)")
     ap.add_argument("--cold", action="store_true",
-                    help="with --only: take the calls in rotation over >= 1 GiB of operand copies")
+                    help="with --only: clear a 512 MiB buffer before every call (for counter runs: the "
+                         "timed cold runs of the bench rotate over operand copies instead)")
     ap.add_argument("--fused", action="store_true", help="with --only: sum the layer copies inside the GEMM")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="with --only: also run a plain device copy of MIB MiB (counter calibration)")
@@ -267,18 +268,19 @@ def main():
     if args.only:
         # one workload's GEMMs (each called --steps times, in turn), for
         # profilers: --only-layers picks the layer count (default: the last of
-        # the workload's list), --only-tile the block shape, --cold takes the
-        # calls in rotation over copies of the operands (the cold protocol),
-        # --fused sums the layer copies in the GEMM
+        # the workload's list), --only-tile the block shape, --cold clears
+        # 512 MiB before every call (operands out of the caches for counter
+        # runs), --fused sums the layer copies in the GEMM
         ow = W[args.only]
         c_only = ow.ca_layers[-1] if args.only_layers is None else args.only_layers
+        flush = torch.empty(512 * 1024 * 1024 // 4, dtype=torch.float32, device=dev) if args.cold else None
         for og in ow.gemms:
             _, _, oA, oB, oC = prepare(og)
-            sets = ColdSets(torch, oA, oB, oC).sets if args.cold else [(oA, oB, oC)]
-            for i in range(args.steps):
-                run_once(*sets[i % len(sets)], ow, c_only, tile=args.only_tile, fused=args.fused)
+            for _ in range(args.steps):
+                if flush is not None:
+                    flush.zero_()
+                run_once(oA, oB, oC, ow, c_only, tile=args.only_tile, fused=args.fused)
             torch.cuda.synchronize()
-            del sets
             log(f"[bench] ran {args.only} {og.M}x{og.N}x{og.K} ca_layers={c_only} order={args.order} "
                 f"{'cold ' if args.cold else ''}{args.steps} times")
             del oA, oB, oC
