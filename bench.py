@@ -130,6 +130,14 @@ def warm_clock(torch, stream, fn, min_ms):
 ROTATION_BYTES = 1 << 30
 
 
+def gpu_backlog(torch, us):
+    """Keep the GPU busy for about `us` microseconds (a spin kernel that touches
+    no memory) while the host enqueues what follows, so that a timed call
+    starts as soon as its start event does: for calls of a few microseconds the
+    host's enqueue time would otherwise sit between the two."""
+    torch.cuda._sleep(int(us * 2000))
+
+
 class ColdSets:
     """The cold protocol of Section IV.A: copies of one GEMM's A, B and C,
     enough of them (at least 2, together at least 1 GiB: past the 256 MiB
@@ -154,6 +162,7 @@ class ColdSets:
             self.next = (self.next + 1) % n
         ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
         for s0, s1 in ev:
+            gpu_backlog(torch, 50)
             s0.record(stream)
             fn(*self.sets[self.next])
             s1.record(stream)
@@ -494,6 +503,7 @@ def main():
                     torch.cuda.synchronize()
                     cold_t += cold_ms(gi, c, args.reps, sched, tile, fused)
                     s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                    gpu_backlog(torch, 40 * args.reps)
                     s.record(stream)
                     for _ in range(args.reps):
                         run_once(a, b, cc, wl, c, sched, tile, fused)
@@ -514,14 +524,18 @@ def main():
                 for gi, x in enumerate(wl.gemms):
                     a, b, cc = ops[gi]
                     cands = []
+                    # the model's choice is timed before and after the candidates
+                    # (mean of the two): the candidates run for a while, and the
+                    # chip's state drifts over that time
+                    run_once(a, b, cc, wl, 0, None, "auto")
+                    mt0 = cold_ms(gi, 0, args.tune_reps, None, "auto")
                     for t in ("128x128", "256x128", "128x256", "256x256"):
                         for c in (1, 2, 4, 8, 16):
                             if c > 1 and c * x.M * x.N * 4 > (2 << 30):
                                 continue
                             run_once(a, b, cc, wl, c, None, t)
                             cands.append((cold_ms(gi, c, args.tune_reps, None, t), t, c))
-                    run_once(a, b, cc, wl, 0, None, "auto")
-                    mt = cold_ms(gi, 0, args.tune_reps, None, "auto")
+                    mt = 0.5 * (mt0 + cold_ms(gi, 0, args.tune_reps, None, "auto"))
                     bt = min(cands)
                     pm = sg.sfc_gemm_plan(x.M, x.N, x.K, 0, "auto")
                     rows.append({"gemm": [x.M, x.N, x.K],
@@ -531,7 +545,8 @@ def main():
                                  "candidates": len(cands)})
                     best_t += bt[0]
                     model_t += mt
-                return {"protocol": f"each candidate: mean of {args.tune_reps} cold calls", "per_gemm": rows,
+                return {"protocol": f"each candidate: mean of {args.tune_reps} cold calls; the model's choice: "
+                                    f"the same, before and after the candidates, averaged", "per_gemm": rows,
                         "model_over_best": round(best_t / model_t, 4)}
 
             per_c = {}

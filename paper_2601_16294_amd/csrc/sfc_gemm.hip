@@ -322,6 +322,15 @@ __device__ __forceinline__ i32x4 make_rsrc_addr(uint64_t a, uint32_t num_records
   r[2] = __builtin_amdgcn_readfirstlane(r[2]);
   return r;
 }
+// The same descriptor in two steps, for code that spreads scalar work thinly:
+// the address words first (wave-uniform values), then the descriptor.
+__device__ __forceinline__ void rsrc_words(uint64_t a, uint32_t& lo, uint32_t& hi) {
+  lo = (uint32_t)a;
+  hi = (uint32_t)(a >> 32) & 0xFFFFu;
+}
+__device__ __forceinline__ i32x4 rsrc_of_words(uint32_t lo, uint32_t hi, uint32_t num_records) {
+  return i32x4{(int)lo, (int)hi, (int)num_records, 0x00020000};
+}
 
 // Per-lane, per-task load offsets (bytes, biased).
 template <int BM, int BN, int NW, int F8>
@@ -682,6 +691,11 @@ __device__ __forceinline__ void ring_group(Acc<BM, BN, NW, F8>& acc, const Frags
                                                                 (F8 - 1) & 1, 0, 127, 0, 127);
   else
     acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(cur.b[j], cur.a[i], acc[i][j], 0, 0, 0);
+  // bf16: the group's other instructions follow its 16-cycle MFMA (left free,
+  // the compiler hoists the next group's reads above it and packs up to 7
+  // instructions between two MFMAs); a 64-cycle fp8 MFMA hides them anyway and
+  // its steps run faster with the compiler's order
+  if constexpr (F8 == 0) __builtin_amdgcn_sched_barrier(0);
   if constexpr (OP == 2 && g == P::G0) {
     // the block's barrier: A block b+1 and B stages x0+2, x0+3 have landed for
     // every wave (only the A block loaded in the A step may be in flight), and
@@ -855,25 +869,34 @@ __device__ __forceinline__ void main_loop_ring(const RingAddr& ra, int nb, int k
   bool mnow = mask_b == 0;                  // block b applies the K mask
   SlotDma da = a_dma(a_nx, D, D < nb ? (uint32_t)kOobOffset : 0u), db0, db1;
 
-  uint32_t lim0, lim1;
+  uint32_t lim0, lim1, lt0, lt1, w_lo, w_hi, a_lim;
+  int x1;
   uint64_t b_nx1;
   for (int b = 0; b < nb; ++b) {
     ring_step<BM, BN, NW, F8, D, 1>(acc, f0, f1, ra.lds0 + la0 + o.a_rd[1], lb1, o, da, da, L, [&]<int g>() {
       if constexpr (g < R::APB) {
         if (mnow && mk[g]) L.a_voff[g] = kOobOffset;
       }
-      if constexpr (g == P1::stage_group(0, 6)) lim0 = b_stage_limit(ra, xb);
-      if constexpr (g == P1::stage_group(1, 6)) db0.rsrc = make_rsrc_addr(b_nx, lim0);
-      if constexpr (g == P1::stage_group(2, 6)) {
+      // the scalar work in pieces of at most three instructions, one piece per
+      // group: an MFMA of 16 cycles hides three others, each one more costs 4
+      constexpr int NS1 = 10;
+      // (the stage limits are b_stage_limit in two selects)
+      if constexpr (g == P1::stage_group(0, NS1)) { lt0 = xb == ra.x_part ? ra.lim_part : (uint32_t)kBias; pin_scalar(lt0); }
+      if constexpr (g == P1::stage_group(1, NS1)) { lim0 = xb < ra.x_part ? (uint32_t)kOobOffset : lt0; pin_scalar(lim0); }
+      if constexpr (g == P1::stage_group(2, NS1)) { rsrc_words(b_nx, w_lo, w_hi); pin_scalar(w_lo); pin_scalar(w_hi); }
+      if constexpr (g == P1::stage_group(3, NS1)) db0.rsrc = rsrc_of_words(w_lo, w_hi, lim0);
+      if constexpr (g == P1::stage_group(4, NS1)) {
         db0.m0 = b_m0w + sb;
         db1.m0 = b_m0w + lb1;
       }
-      if constexpr (g == P1::stage_group(3, 6)) lim1 = b_stage_limit(ra, xb + 1);
-      if constexpr (g == P1::stage_group(4, 6)) b_nx1 = b_nx + ra.b_step;
-      if constexpr (g == P1::stage_group(5, 6)) db1.rsrc = make_rsrc_addr(b_nx1, lim1);
+      if constexpr (g == P1::stage_group(5, NS1)) { x1 = xb + 1; lt1 = x1 == ra.x_part ? ra.lim_part : (uint32_t)kBias; pin_scalar(lt1); }
+      if constexpr (g == P1::stage_group(6, NS1)) { lim1 = x1 < ra.x_part ? (uint32_t)kOobOffset : lt1; pin_scalar(lim1); }
+      if constexpr (g == P1::stage_group(7, NS1)) { b_nx1 = b_nx + ra.b_step; pin_scalar(b_nx1); }
+      if constexpr (g == P1::stage_group(8, NS1)) { rsrc_words(b_nx1, w_lo, w_hi); pin_scalar(w_lo); pin_scalar(w_hi); }
+      if constexpr (g == P1::stage_group(9, NS1)) db1.rsrc = rsrc_of_words(w_lo, w_hi, lim1);
     });
     ring_step<BM, BN, NW, F8, D, 2>(acc, f1, f0, ra.lds0 + la1 + o.a_rd[0], lb2, o, db0, db1, L, [&]<int g>() {
-      if constexpr (g == P2::stage_group(0, 5)) {
+      if constexpr (g == P2::stage_group(0, 8)) {
         const uint32_t t = la0;
         la0 = la1;
         la1 = la2;
@@ -888,7 +911,7 @@ __device__ __forceinline__ void main_loop_ring(const RingAddr& ra, int nb, int k
           la4 = t;
         }
       }
-      if constexpr (g == P2::stage_group(1, 5)) {
+      if constexpr (g == P2::stage_group(1, 8)) {
         if constexpr (R::NB == 4) {
           sb ^= 2 * BB;
           lb1 ^= 2 * BB;
@@ -899,18 +922,22 @@ __device__ __forceinline__ void main_loop_ring(const RingAddr& ra, int nb, int k
           lb2 = lb2 + 2 * BB == (uint32_t)R::NB * BB ? 0u : lb2 + 2 * BB;
         }
       }
-      if constexpr (g == P2::stage_group(2, 5)) {
+      if constexpr (g == P2::stage_group(2, 8)) {
         a_nx += kBK * 2;
         pin_scalar(a_nx);
       }
-      if constexpr (g == P2::stage_group(3, 5)) {
-        da.rsrc = make_rsrc_addr(a_nx, b + 1 + D < nb ? (uint32_t)kOobOffset : 0u);
+      if constexpr (g == P2::stage_group(3, 8)) { a_lim = b + 1 + D < nb ? (uint32_t)kOobOffset : 0u; pin_scalar(a_lim); }
+      if constexpr (g == P2::stage_group(4, 8)) { rsrc_words(a_nx, w_lo, w_hi); pin_scalar(w_lo); pin_scalar(w_hi); }
+      if constexpr (g == P2::stage_group(5, 8)) {
+        da.rsrc = rsrc_of_words(w_lo, w_hi, a_lim);
         da.m0 = a_m0w + (D == 2 ? la2 : D == 3 ? la3 : la4);
       }
-      if constexpr (g == P2::stage_group(4, 5)) {
+      if constexpr (g == P2::stage_group(6, 8)) {
         b_nx += 2 * ra.b_step;
-        xb += 2;
         pin_scalar(b_nx);
+      }
+      if constexpr (g == P2::stage_group(7, 8)) {
+        xb += 2;
         pin_scalar(xb);
         mnow = b + 1 == mask_b;
       }
