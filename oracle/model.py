@@ -7,7 +7,7 @@ Eq. 1 T = max(G*gamma, beta*(S_A + S_B)) when both panels come from slow
 memory (Eq. 2-4 when one or both are already in fast memory), sums these over
 the critical path, adds the reads/writes of C and, for 2.5D/3D runs, of the C
 copies, and takes the decomposition with the smallest time (Section III.C,
-second option).  The reading for this GPU (listed in the design doc):
+second option).  The reading for this GPU:
 
 * a core is a CU; it holds up to ``occ`` persistent workgroups; a workgroup
   gets 1/w of its CU's MFMA rate (gamma = w / (flops per clock x rate)), where

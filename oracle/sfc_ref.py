@@ -23,7 +23,7 @@ vector along which the walk advances and a "minor" vector across it):
   (and the side longer than 2) it is grown by one cell so that sub-walks end on
   the corner where their successor starts.
 
-Readings of the paper (all listed in the design doc): the x coordinate is the block
+Readings of the paper where it leaves a choice: the x coordinate is the block
 row im and y the block column in; the longer side is the major axis at the top
 level, ties going to x; the order is returned as ``cell = im * gn + in``.
 

@@ -1,8 +1,8 @@
 """Pins of the block-shape / layer-count model oracle (oracle/model.py).
 
 The model is the paper's Section III.B roofline (Eq. 1-4) evaluated over the
-decompositions (Section III.C, second option), read for the GPU as listed in
-the design doc.  The pins: Eq. 1 on hand-computed blocks, one whole estimate worked
+decompositions (Section III.C, second option), read for the GPU as the
+oracle's docstring states.  The pins: Eq. 1 on hand-computed blocks, one whole estimate worked
 out by hand, the M <-> N symmetry of the model, and the two facts the paper's
 CA scheme rests on (Section II.C, Section IV.B): a K-dominant GEMM whose C grid
 cannot fill the machine needs layers, a large square one does not.
