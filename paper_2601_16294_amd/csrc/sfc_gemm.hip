@@ -518,12 +518,14 @@ __device__ __forceinline__ void dma_all(const SlotDma& d, const RingLanes<BM, BN
 }
 
 // Instruction plan of one 32-deep step: FM*FN groups, each one MFMA of the
-// current fragments plus at most one fragment read for the next step and at
-// most one load operation.  With one wave per SIMD a wave issues one
-// instruction every 4 cycles, so a 16-cycle MFMA hides three others; two LDS
-// reads in one group already cost extra cycles (both measured on gfx950).
+// current fragments plus at most one fragment read for the next step (two in
+// the shorter steps of the smaller bf16 blocks) and at most one load
+// operation.  With one wave per SIMD a wave issues one instruction every 4
+// cycles, so a 16-cycle MFMA hides three others; two LDS reads in one group
+// already cost extra cycles (both measured on gfx950).
 //   reads:  A0, B0 low, B0 high, B1 low, .., B(FN-1) high, A1, .., A(FM-1)
-//           (the order the next step's MFMAs consume them), spread evenly;
+//           (the order the next step's MFMAs consume them), spread evenly over
+//           the first half of the step (bf16) or the whole step (fp8);
 //   loads:  each load pair becomes three operations (set M0, load, load) in
 //           consecutive groups from evenly spaced starting groups, so that the
 //           MFMA between M0 and the first load covers the wait M0 needs; a
@@ -548,7 +550,13 @@ struct StepPlan {
   // whole pairs: one operation per pair (M0, a wait state and both loads)
   static constexpr bool WHOLE = 3 * NP > G - G0;
   static constexpr int ND = WHOLE ? NP : 3 * NP;
-  static constexpr int read_group(int r) { return G0 + (r * (G - G0)) / NR; }
+  // bf16 reads run over the first half of the step's groups: the next step's
+  // first MFMAs need them, and the LDS returns them late under the step's own
+  // loads (2 % faster on 8192^3 than spread over the whole step, measured);
+  // fp8 spreads them over the whole step
+  static constexpr int read_group(int r) {
+    return F8 ? G0 + (r * (G - G0)) / NR : G0 + (r * (G - G0)) / (2 * NR);
+  }
   static constexpr int dma_group(int o) {
     if (WHOLE) return G0 + ((2 * o + 1) * (G - G0)) / (2 * NP);
     int g = G0 - 1;
@@ -590,9 +598,9 @@ struct StepPlan {
       if (dma_group(WHOLE ? q : 3 * q + 1) <= 2 * q + 1) return false;
     return true;
   }
-  // bf16: at most one read beside each 16-cycle MFMA; fp8: up to three beside
+  // bf16: at most two reads beside each 16-cycle MFMA; fp8: up to three beside
   // each 64-cycle MFMA
-  static_assert(NR <= (F8 ? 3 : 1) * (G - G0), "reads per group");
+  static_assert(F8 ? NR <= 3 * (G - G0) : NR <= G - G0, "reads per group");
   static_assert(ND == 0 || dma_group(ND - 1) < G, "loads fit in the step");
   static_assert(OP != 1 || a_loads_after_masks(), "A loads after their K-mask selects");
 };
