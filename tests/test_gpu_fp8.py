@@ -97,6 +97,17 @@ def test_auto_block_shape_follows_the_model(M, N, K, c):
     assert plan["layers"] == min(best[1], -(-K // 128))
 
 
+@pytest.mark.parametrize("tile", ["auto", "256x256", "128x256"])
+@pytest.mark.parametrize("out", ["f32", "bf16"])
+def test_k_zero_writes_zeros(tile, out):
+    M, N = 70, 96
+    A = np.zeros((M, 16), np.uint8)
+    B = np.zeros((16, N), np.uint8)
+    for c in (1, 0):
+        C = to_host(run8(A, B, M, N, 0, out, c, tile=tile))
+        assert (C == 0).all(), (tile, out, c)
+
+
 @pytest.mark.parametrize("c", [1, 2, 5])
 def test_integer_inputs_exact(c):
     M, N, K = 300, 272, 1040
