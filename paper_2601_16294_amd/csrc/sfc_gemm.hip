@@ -11,8 +11,9 @@
 // fp32 workspace layer that a separate reduction sums.
 //
 // Mapping to the chip:
-//   * one workgroup = 4 waves (one per SIMD; 2 x 2, or 1 x 4 for 128x256
-//     blocks), each wave owning its sub-block as 16x16 fp32 MFMA accumulators;
+//   * one workgroup = 4 waves (one per SIMD; 1 x 4 for blocks 256 columns
+//     wide, except fp8 256x256, else 2 x 2), each wave owning its sub-block as
+//     16x16 fp32 MFMA accumulators;
 //   * the grid is persistent: P workgroups, P = CUs x occupancy, each looping
 //     over tasks.  Hardware deals workgroup b to chiplet (XCD) b % 8; ranks are
 //     renumbered so that each XCD's workgroups hold consecutive ranks, and with
@@ -151,13 +152,17 @@ __device__ __forceinline__ void wait_lds_all() { asm volatile("s_waitcnt lgkmcnt
 // consecutive columns 4*(l/16) .. +3.
 // NW = 4 waves per workgroup (one per SIMD) in a WGM x WGN grid.  A wave's
 // fragment reads per 32-deep step are FM b128 reads of A and 2*FN transposing
-// reads of B, so the grid keeps the wave sub-block at most twice as wide as
-// tall: 2 x 2 waves, except 1 x 4 for 128x256 blocks (128x64 per wave).
+// reads of B.  A transposing read takes about twice the LDS time of a b128
+// read per byte and, unlike b128 reads, slows the global-to-LDS loads that run
+// beside it, so blocks 256 columns wide put the 4 waves side by side (1 x 4:
+// 128x64 or, for bf16 256x256, 256x64 per wave, a quarter of B each) and the
+// narrower blocks keep 2 x 2.  (fp8 256x256 blocks stay 2 x 2: 1 x 4 measured
+// 1.5 % slower there.)
 template <int BM, int BN, int NW, int F8>
 struct Tile {
   static_assert(NW == 4, "4 waves");
   static constexpr int THREADS = NW * 64;
-  static constexpr int WGM = (BM == 128 && BN == 256) ? 1 : 2;  // waves along M
+  static constexpr int WGM = (BN == 256 && (BM == 128 || F8 == 0)) ? 1 : 2;  // waves along M
   static constexpr int WGN = NW / WGM;                // waves along N
   static constexpr int WTM = BM / WGM, WTN = BN / WGN;  // wave sub-block
   // fragments per wave: 16x16 (bf16, MFMA 16x16x32) or 32x32 (fp8, MFMA 32x32x64)
