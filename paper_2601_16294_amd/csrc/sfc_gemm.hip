@@ -549,18 +549,21 @@ struct StepPlan {
   // the B step opens with G0 groups of MFMAs alone and then waits at the
   // block's barrier: those MFMAs need nothing the barrier publishes, and they
   // keep the matrix core busy while the waves meet and while the A step's last
-  // fragment reads (which the barrier waits for) complete; steps of 32 or more
-  // MFMAs open with 4 (measured best of 2, 4, 6, 8), shorter ones with 2
-  static constexpr int G0 = OP == 2 ? (T::FM * T::FN >= 32 ? 4 : 2) : 0;
+  // fragment reads (which the barrier waits for) complete; steps of 32 MFMAs
+  // open with 4 (measured best of 2, 4, 6, 8), the 64-MFMA steps of bf16
+  // 256x256 blocks and shorter steps with 2
+  static constexpr int G0 = OP == 2 ? (T::FM * T::FN == 32 ? 4 : 2) : 0;
   // whole pairs: one operation per pair (M0, a wait state and both loads)
   static constexpr bool WHOLE = 3 * NP > G - G0;
   static constexpr int ND = WHOLE ? NP : 3 * NP;
-  // bf16 reads run over the first half of the step's groups: the next step's
-  // first MFMAs need them, and the LDS returns them late under the step's own
-  // loads (2 % faster on 8192^3 than spread over the whole step, measured);
-  // fp8 spreads them over the whole step
+  // bf16 reads of 32-group steps run over the first half of the step's groups:
+  // the next step's first MFMAs need them, and the LDS returns them late under
+  // the step's own loads (2 % faster on 8192^3 than spread over the whole step
+  // with 2 x 2 waves, measured); fp8 and the 64-group steps of bf16 256x256
+  // blocks (1 x 4 waves, fewer transposing reads) spread them over the whole
+  // step (0.2-1.6 % faster there than the first half, measured)
   static constexpr int read_group(int r) {
-    return F8 ? G0 + (r * (G - G0)) / NR : G0 + (r * (G - G0)) / (2 * NR);
+    return (F8 || G >= 64) ? G0 + (r * (G - G0)) / NR : G0 + (r * (G - G0)) / (2 * NR);
   }
   static constexpr int dma_group(int o) {
     if (WHOLE) return G0 + ((2 * o + 1) * (G - G0)) / (2 * NP);
